@@ -1,0 +1,165 @@
+"""Seeded synthetic inputs shared by the oracle-side tests and the HIP path.
+
+This module only draws random numbers and rounds them to bfloat16 bit
+patterns.  It contains none of the attention arithmetic: the oracle and the
+HIP library each consume the arrays it returns on their own.
+
+Workload shapes follow Qwen2.5-VL-3B/7B attention layers (post-RoPE Q/K/V,
+grouped-query heads), which is what the streaming LLM prefill of the paper
+(Sec. 3, "LLM Prefilling and Decoding") runs on.  Real video benchmarks are
+not available, so Gaussian tensors stand in for the activations.
+
+Draw order for one chunk is fixed: Q, K_chunk, V_chunk, sink_K, sink_V,
+hist_K, hist_V.  Every tensor is drawn as float32 standard normal times a
+scale, then rounded to bfloat16 with round-to-nearest-even.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = [
+    "f32_to_bf16_bits",
+    "ChunkShape",
+    "ChunkInputs",
+    "make_chunk_inputs",
+    "ragged_chunk_lengths",
+    "stream_chunk",
+    "CONFIGS",
+]
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (round-to-nearest-even); return uint16 bits.
+
+    Inputs are finite Gaussian draws, so no NaN/Inf handling is needed.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    b = x.view(np.uint32).astype(np.uint64)
+    lsb = (b >> np.uint64(16)) & np.uint64(1)
+    r = (b + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
+    return r.astype(np.uint16)
+
+
+@dataclass(frozen=True)
+class ChunkShape:
+    """Shape of one chunk-prefill attention call.
+
+    hist_len is the linear count of visual tokens appended before this chunk;
+    window is the number of most recent history tokens visible (-1: all).
+    """
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    sink_len: int
+    ring_slots: int
+    hist_len: int
+    window: int
+    chunk_len: int
+
+    @property
+    def visible_window(self) -> int:
+        if self.window < 0:
+            return self.hist_len
+        return min(self.window, self.hist_len)
+
+    @property
+    def hist_stored(self) -> int:
+        """History positions that are still resident in the ring."""
+        return min(self.hist_len, self.ring_slots)
+
+
+@dataclass
+class ChunkInputs:
+    """bf16 bit patterns (uint16) for one chunk call.
+
+    hist_k/hist_v hold linear history positions [hist_len - hist_stored,
+    hist_len), oldest first.  Placing them into ring slots is the caller's job.
+    """
+    shape: ChunkShape
+    q: np.ndarray          # [C, Hq, d]
+    k_chunk: np.ndarray    # [C, Hkv, d]
+    v_chunk: np.ndarray    # [C, Hkv, d]
+    sink_k: np.ndarray     # [S, Hkv, d]
+    sink_v: np.ndarray     # [S, Hkv, d]
+    hist_k: np.ndarray     # [min(H, R), Hkv, d]
+    hist_v: np.ndarray     # [min(H, R), Hkv, d]
+    hist_first: int = field(default=0)   # linear position of hist_k[0]
+
+
+def _draw(rng: np.random.Generator, shape, sigma: float) -> np.ndarray:
+    return f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(sigma))
+
+
+def make_chunk_inputs(shape: ChunkShape, seed=0, family: str = "F1") -> ChunkInputs:
+    """Draw all tensors of one chunk call.
+
+    family "F1": Q, K, V ~ N(0,1)/sqrt(head_dim) (the literal workload recipe).
+    family "F2": Q, K ~ 2*N(0,1), V ~ N(0,1): logits of standard deviation 4
+                 and O(1) outputs, used for the binding parity tolerance.
+    """
+    d = shape.head_dim
+    if family == "F1":
+        sq = sk = sv = 1.0 / np.sqrt(d)
+    elif family == "F2":
+        sq, sk, sv = 2.0, 2.0, 1.0
+    else:
+        raise ValueError(f"unknown input family {family!r}")
+    rng = np.random.Generator(np.random.PCG64(seed))
+    C, Hq, Hkv, S = shape.chunk_len, shape.num_q_heads, shape.num_kv_heads, shape.sink_len
+    n_hist = shape.hist_stored
+    q = _draw(rng, (C, Hq, d), sq)
+    kc = _draw(rng, (C, Hkv, d), sk)
+    vc = _draw(rng, (C, Hkv, d), sv)
+    sk_ = _draw(rng, (S, Hkv, d), sk)
+    sv_ = _draw(rng, (S, Hkv, d), sv)
+    hk = _draw(rng, (n_hist, Hkv, d), sk)
+    hv = _draw(rng, (n_hist, Hkv, d), sv)
+    return ChunkInputs(shape, q, kc, vc, sk_, sv_, hk, hv, hist_first=shape.hist_len - n_hist)
+
+
+def ragged_chunk_lengths(n_chunks: int = 64, lo: int = 256, hi: int = 1024, seed: int = 0) -> np.ndarray:
+    """Retained-token counts per chunk, uniform in [lo, hi] (token-dropping output)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.integers(lo, hi + 1, n_chunks)
+
+
+def stream_chunk(t: int, chunk_len: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                 seed: int = 0, family: str = "F1"):
+    """Q/K/V bits of streaming chunk t: drawn from PCG64([seed, t]) in order Q, K, V."""
+    d = head_dim
+    if family == "F1":
+        sq = sk = sv = 1.0 / np.sqrt(d)
+    else:
+        sq, sk, sv = 2.0, 2.0, 1.0
+    rng = np.random.Generator(np.random.PCG64([seed, t]))
+    q = _draw(rng, (chunk_len, num_q_heads, d), sq)
+    k = _draw(rng, (chunk_len, num_kv_heads, d), sk)
+    v = _draw(rng, (chunk_len, num_kv_heads, d), sv)
+    return q, k, v
+
+
+def stream_sink(sink_len: int, num_kv_heads: int, head_dim: int, seed: int = 0, family: str = "F1"):
+    """Sink K/V bits for a stream, drawn from PCG64([seed, 1 << 20])."""
+    d = head_dim
+    sk, sv = (1.0 / np.sqrt(d),) * 2 if family == "F1" else (2.0, 1.0)
+    rng = np.random.Generator(np.random.PCG64([seed, 1 << 20]))
+    return _draw(rng, (sink_len, num_kv_heads, d), sk), _draw(rng, (sink_len, num_kv_heads, d), sv)
+
+
+# Workload shapes (one attention layer each).  The ring holds exactly W slots.
+CONFIGS = {
+    # tiny: 2/1 heads, d 64, sink 16, W = R = 256, chunk 64; ring write pointer at 200.
+    "tiny": ChunkShape(2, 1, 64, 16, 256, 456, 256, 64),
+    "tiny_partial": ChunkShape(2, 1, 64, 16, 256, 200, 256, 64),
+    # Qwen2.5-VL-3B layer: 16/2 heads, d 128, sink 64, W = R = 8192, chunk 1024.
+    "3b": ChunkShape(16, 2, 128, 64, 8192, 8192, 8192, 1024),
+    "3b_wrap": ChunkShape(16, 2, 128, 64, 8192, 5 * 8192 + 777, 8192, 1024),
+    # Qwen2.5-VL-7B layer: 28/4 heads, d 128, sink 64, W = R = 16384, chunk 2048.
+    "7b": ChunkShape(28, 4, 128, 64, 16384, 16384, 16384, 2048),
+    "7b_wrap": ChunkShape(28, 4, 128, 64, 16384, 5 * 16384 + 777, 16384, 2048),
+    # full history (65536 tokens) vs bounded W = 8192 at 3B heads, chunk 2048.
+    "full": ChunkShape(16, 2, 128, 64, 65536, 65536, -1, 2048),
+    "full_bounded": ChunkShape(16, 2, 128, 64, 65536, 65536, 8192, 2048),
+}
