@@ -1,0 +1,257 @@
+#!/usr/bin/env python3
+"""Benchmark of the bounded chunk-prefill hot path on one MI355X.
+
+One step = one streaming chunk through the whole path: bounded attention of
+the chunk over [sink | W newest history tokens via the ring | causal chunk],
+then the ring append of the chunk's K/V.  The history length advances by
+the chunk length every step, so each step reads a different window phase
+(the ring wraps inside key tiles).  Inputs are resident in HBM before the
+timed region.
+
+Default workload: one Qwen2.5-VL-7B-shaped attention layer -- 28 query /
+4 KV heads, head_dim 128, sink 64, W = R = 16384, chunk 2048 -- the shape
+the >= 50 % of bf16 MFMA peak target is stated on.  `--workload` selects the
+others (3b, full, full_bounded, stream).
+
+Prints one JSON line.  `value` is algorithmic TFLOP/s over whole steps
+(attention + append); `roofline` prices the attention kernel alone from
+HIP events on its stream; `cpu_baseline` times the fp64 oracle on a bounded
+sample of rows of the same chunk on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_HBM_GBS = 8000.0
+
+
+def attn_flops(C, S, Wv, Hq, D, rows=None):
+    """Algorithmic flops: 4*d per (query row, visible key) per head; masked pairs excluded."""
+    r = np.arange(C) if rows is None else np.asarray(rows)
+    return float(4 * Hq * D * np.sum(S + Wv + r + 1, dtype=np.float64))
+
+
+def workload_shape(name):
+    from synth import CONFIGS
+    table = {"7b": "7b_wrap", "3b": "3b_wrap", "full": "full", "full_bounded": "full_bounded"}
+    return CONFIGS[table[name]]
+
+
+DESCR = {
+    "7b": "qwen2.5-vl-7b layer chunk prefill: 28q/4kv heads, d128, sink 64, W=R=16384, chunk 2048",
+    "3b": "qwen2.5-vl-3b layer chunk prefill: 16q/2kv heads, d128, sink 64, W=R=8192, chunk 1024",
+    "full": "3b heads, full history 65536 + sink 64, chunk 2048 (unbounded control)",
+    "full_bounded": "3b heads, history 65536 + sink 64, W=8192, chunk 2048",
+    "stream": "3b heads, 64 chunks ragged in [256,1024], sink 64, W=R=8192, attend then append",
+}
+
+
+def cpu_baseline(inp, n_rows, seed=0):
+    """Time the fp64 oracle on `n_rows` rows (all heads) of the same chunk."""
+    import oracle
+    from tests._util import to_f64
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    sh = inp.shape
+    rows = np.linspace(0, sh.chunk_len - 1, n_rows).round().astype(np.int64)
+    x = to_f64(inp)
+    t0 = time.perf_counter()
+    oracle.chunk_prefill_attention(**x, rows=rows)
+    dt = time.perf_counter() - t0
+    fl = attn_flops(sh.chunk_len, sh.sink_len, sh.visible_window, sh.num_q_heads, sh.head_dim, rows)
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n_rows} evenly spaced rows of the chunk x all {sh.num_q_heads} heads "
+                      f"({fl / 1e9:.1f} GFLOP fp64) in {dt:.1f} s",
+            "tokens_per_s": n_rows / dt}
+
+
+def _dev(torch, bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def run_chunk_workload(args, torch, vico):
+    from synth import make_chunk_inputs
+    sh = workload_shape(args.workload)
+    inp = make_chunk_inputs(sh, seed=0, family="F1")
+    q, kc, vc = _dev(torch, inp.q), _dev(torch, inp.k_chunk), _dev(torch, inp.v_chunk)
+    sk, sv = _dev(torch, inp.sink_k), _dev(torch, inp.sink_v)
+    C, S, R, Hq, Hkv, D, W = (sh.chunk_len, sh.sink_len, sh.ring_slots, sh.num_q_heads, sh.num_kv_heads,
+                              sh.head_dim, sh.window)
+    # the resident history enters the ring through the library's own append
+    rk = torch.zeros((R, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    rv = torch.zeros_like(rk)
+    vico.vico_kv_append(_dev(torch, inp.hist_k), _dev(torch, inp.hist_v), rk, rv, inp.hist_first)
+    out = torch.empty((C, Hq, D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((Hq, C), dtype=torch.float32, device="cuda")
+    H0 = sh.hist_len
+    full = W < 0
+    n_total = args.warmup + args.steps
+    plans = []
+    for i in range(n_total):
+        H = H0 if full else H0 + i * C          # full-history control keeps its history fixed
+        plans.append((H,) + vico.vico_attn_plan(C, S, R, H, W, Hq, Hkv, D))
+    wb = max(p[2] for p in plans)
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+
+    def step(i, events=None):
+        H = plans[i][0]
+        if events:
+            events[0].record(stream)
+        vico.vico_chunk_prefill_attn(q, kc, vc, sk, sv, rk, rv, H, W, out, lse=lse, workspace=ws, stream=stream)
+        if events:
+            events[1].record(stream)
+        if not full:
+            vico.vico_kv_append(kc, vc, rk, rv, H, stream=stream)
+        if events:
+            events[2].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for j in range(args.steps):
+        step(args.warmup + j, ev[j])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    attn_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    app_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    assert torch.isfinite(out.float()).all().item(), "non-finite attention output"
+
+    Wv = sh.visible_window
+    fl = attn_flops(C, S, Wv, Hq, D)
+    ms_step = elapsed * 1e3 / args.steps
+    achieved = fl / (attn_ms.mean() * 1e-3) / 1e12
+    app_bytes = 2 * 2 * C * Hkv * D * 2          # K and V, read + write
+    res = {
+        "metric": "chunk-prefill attention TFLOP/s (% bf16 MFMA peak) + visual tokens/s per layer",
+        "value": round(fl * args.steps / elapsed / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": DESCR[args.workload], "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D,
+                   "sink": S, "window": W, "ring_slots": R, "chunk": C, "hist_start": H0,
+                   "splits": plans[-1][1], "out_dtype": "bf16", "inputs": "N(0,1)/sqrt(d) bf16, seed 0"},
+        "pct_peak": round(100 * fl * args.steps / elapsed / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "visual_tokens_per_s": round(C * args.steps / elapsed, 1),
+        "attn_ms_mean": round(float(attn_ms.mean()), 4),
+        "attn_ms_median": round(float(np.median(attn_ms)), 4),
+        "append_ms_mean": round(float(app_ms.mean()), 4) if not full else None,
+        "append_GBps": round(app_bytes / (app_ms.mean() * 1e-3) / 1e9, 1) if not full else None,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": args.traffic_bytes, "kernel": "attn_fwd_kernel<128>",
+                     "flops_per_launch": fl},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_rows)
+    return res
+
+
+def run_stream_workload(args, torch, vico):
+    """64 ragged chunks at the 3B shape: per-chunk latency vs chunk index."""
+    from synth import ragged_chunk_lengths, stream_chunk, stream_sink
+    dev = lambda bits: _dev(torch, bits)
+    Hq, Hkv, D, S, W, R = 16, 2, 128, 64, 8192, 8192
+    counts = ragged_chunk_lengths(64, 256, 1024, seed=0)
+    res_all = {}
+    for mode, window, slots in (("bounded", W, R), ("full", -1, int(counts.sum()))):
+        sk_b, sv_b = stream_sink(S, Hkv, D, seed=0)
+        sk, sv = dev(sk_b), dev(sv_b)
+        rk = torch.zeros((slots, Hkv, D), dtype=torch.bfloat16, device="cuda")
+        rv = torch.zeros_like(rk)
+        chunks = [tuple(dev(x) for x in stream_chunk(t, int(c), Hq, Hkv, D, seed=0)) for t, c in enumerate(counts)]
+        starts = np.concatenate([[0], np.cumsum(counts)])
+        wb = max(vico.vico_attn_plan(int(c), S, slots, int(starts[t]), window, Hq, Hkv, D)[1]
+                 for t, c in enumerate(counts))
+        ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+        outs = [torch.empty((int(c), Hq, D), dtype=torch.bfloat16, device="cuda") for c in counts]
+        stream = torch.cuda.current_stream()
+        lat = np.zeros((args.steps, len(counts)))
+        for rep in range(args.warmup + args.steps):
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                   torch.cuda.Event(enable_timing=True)) for _ in counts]
+            for t, c in enumerate(counts):
+                q, k, v = chunks[t]
+                ev[t][0].record(stream)
+                vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, int(starts[t]), window, outs[t],
+                                             workspace=ws, stream=stream)
+                ev[t][1].record(stream)
+                vico.vico_kv_append(k, v, rk, rv, int(starts[t]), stream=stream)
+                ev[t][2].record(stream)
+            torch.cuda.synchronize()
+            if rep >= args.warmup:
+                lat[rep - args.warmup] = [e[0].elapsed_time(e[2]) for e in ev]
+        med = np.median(lat, axis=0)
+        flops = np.array([attn_flops(int(c), S, min(int(starts[t]), W) if window >= 0 else int(starts[t]), Hq, D)
+                          for t, c in enumerate(counts)])
+        # latency = a + b * flops + c * t over the chunks whose window is full
+        t_idx = np.arange(len(counts))
+        sel = starts[:-1] >= W if window >= 0 else np.ones(len(counts), bool)
+        X = np.stack([np.ones(sel.sum()), flops[sel], t_idx[sel]], 1)
+        coef = np.linalg.lstsq(X, med[sel], rcond=None)[0]
+        res_all[mode] = {
+            "per_chunk_ms": [round(float(x), 4) for x in med],
+            "tokens_per_s": round(float(counts.sum() / (med.sum() * 1e-3)), 1),
+            "tflops_per_chunk": [round(float(f / (m * 1e-3) / 1e12), 1) for f, m in zip(flops, med)],
+            "drift_ms_over_64_chunks": round(float(coef[2] * 63), 4),
+            "mean_ms": round(float(med.mean()), 4),
+        }
+    b = res_all["bounded"]
+    return {
+        "metric": "chunk-prefill attention TFLOP/s (% bf16 MFMA peak) + visual tokens/s per layer",
+        "value": b["tokens_per_s"], "unit": "visual tokens/s per layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(sum(b["per_chunk_ms"]), 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": DESCR["stream"], "chunks": len(counts), "tokens": int(counts.sum())},
+        "stream": res_all,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--traffic-bytes", type=float, default=None,
+                    help="HBM bytes per attention launch from rocprofv3 FETCH_SIZE+WRITE_SIZE, if measured")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; the multi-GPU layout (KV-head sharding) is "
+              "described in the design notes but not built", file=sys.stderr)
+        sys.exit(2)
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import torch
+    import paper_2606_19849_amd as vico
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    vico.load_library()
+    if args.workload == "stream":
+        res = run_stream_workload(args, torch, vico)
+    else:
+        res = run_chunk_workload(args, torch, vico)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,34 @@
+"""Bounded chunk-prefill attention and ring-buffer KV append for MI355X (gfx950).
+
+The hot path of ViCoStream's bounded visual attention (Sec. 3, "LLM
+Prefilling and Decoding"): each video chunk's retained visual tokens attend
+to a sink prefix, the W newest cached visual tokens and themselves
+(causally) under grouped-query attention; the chunk's K/V then enter a
+ring-buffer cache.  All arithmetic runs in the hand-written HIP kernels of
+libvico.so (C ABI in include/vico.h); this package only marshals arguments.
+"""
+from ._binding import (
+    VICO_DTYPE_BF16,
+    VICO_DTYPE_F32,
+    VICO_FULL_HISTORY,
+    VicoError,
+    load_library,
+    header_functions,
+    vico_attn_plan,
+    vico_attn_workspace_bytes,
+    vico_chunk_prefill_attn,
+    vico_kv_append,
+)
+
+__all__ = [
+    "VICO_DTYPE_BF16",
+    "VICO_DTYPE_F32",
+    "VICO_FULL_HISTORY",
+    "VicoError",
+    "load_library",
+    "header_functions",
+    "vico_attn_plan",
+    "vico_attn_workspace_bytes",
+    "vico_chunk_prefill_attn",
+    "vico_kv_append",
+]

@@ -1,0 +1,201 @@
+// Host side of the C ABI declared in include/vico.h: argument validation,
+// launch planning and error mapping.  Nothing here allocates device memory;
+// every buffer, the workspace included, belongs to the caller.
+
+#include <math.h>
+#include <stdint.h>
+
+#include "vico.h"
+#include "vico_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int64_t kMaxChunk = int64_t(1) << 20;
+constexpr int64_t kMaxKeys = int64_t(1) << 30;
+constexpr int kMaxHeads = 1024;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+struct Shape {
+  int C, S, R, Wv, ws, Hq, Hkv, D, splits;
+  int64_t ws_bytes;
+};
+
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+int plan_splits(int C, int S, int Wv, int Hq, int D, int request) {
+  const int BN = vico::key_tile(D);
+  const int64_t n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
+  const int64_t wgs = int64_t(Hq) * n_rt;
+  const int64_t tiles = (int64_t(S) + Wv + C + BN - 1) / BN;
+  const int64_t cap = tiles < vico::kMaxSplits ? tiles : vico::kMaxSplits;
+  if (request > 0) return (int)(request < cap ? request : cap);
+  // Split only while the grid stays within one round of resident work-groups
+  // and every split keeps at least 16 key tiles.
+  int ns = 1;
+  while (ns * 2 <= cap && wgs * ns * 2 <= int64_t(vico::kNumCUs) * vico::kWgPerCU && tiles >= 16 * ns * 2) ns *= 2;
+  return ns;
+}
+
+// Validates everything the attention call and the planner share.
+int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int32_t Hq, int32_t Hkv,
+                     int32_t D, int32_t splits, Shape* sh) {
+  if (C < 0 || S < 0 || R < 0 || H < 0 || W < -1 || splits < 0) return VICO_ERR_INVALID_ARG;
+  if (Hq < 1 || Hkv < 1 || Hq > kMaxHeads || Hq % Hkv != 0) return VICO_ERR_INVALID_ARG;
+  if (D != 64 && D != 128) return VICO_ERR_UNSUPPORTED;
+  if (C > kMaxChunk || S > kMaxChunk) return VICO_ERR_INVALID_ARG;
+  const int64_t wv = (W < 0) ? H : (W < H ? W : H);
+  if (wv > R) return VICO_ERR_CAPACITY;
+  if (int64_t(S) + wv + C > kMaxKeys) return VICO_ERR_INVALID_ARG;
+  sh->C = C; sh->S = S; sh->R = R; sh->Wv = (int)wv;
+  sh->ws = R > 0 ? (int)((H - wv) % R) : 0;
+  sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;
+  sh->splits = C > 0 ? plan_splits(C, S, (int)wv, Hq, D, splits) : 1;
+  sh->ws_bytes = sh->splits > 1
+                     ? align256(int64_t(4) * sh->splits * Hq * C * D) + int64_t(4) * sh->splits * Hq * C
+                     : 0;
+  return VICO_OK;
+}
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return VICO_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* vico_status_str(int status) {
+  switch (status) {
+    case VICO_OK: return "ok";
+    case VICO_ERR_INVALID_ARG: return "invalid argument";
+    case VICO_ERR_UNSUPPORTED: return "unsupported head_dim or dtype";
+    case VICO_ERR_CAPACITY: return "ring buffer too small for the window or the chunk";
+    case VICO_ERR_MISALIGNED: return "pointer not 16-byte aligned";
+    case VICO_ERR_WORKSPACE: return "workspace missing or too small";
+    case VICO_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int vico_last_hip_error(void) { return g_last_hip_error; }
+
+int vico_attn_plan(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len, int64_t window,
+                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t num_splits,
+                   int32_t* num_splits_out, int64_t* workspace_bytes_out) {
+  Shape sh;
+  const int st = check_attn_shape(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads,
+                                  head_dim, num_splits, &sh);
+  if (st != VICO_OK) return st;
+  if (num_splits_out) *num_splits_out = sh.splits;
+  if (workspace_bytes_out) *workspace_bytes_out = sh.ws_bytes;
+  return VICO_OK;
+}
+
+int64_t vico_attn_workspace_bytes(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len,
+                                  int64_t window, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                  int32_t num_splits) {
+  int64_t b = 0;
+  const int st = vico_attn_plan(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads,
+                                head_dim, num_splits, nullptr, &b);
+  return st != VICO_OK ? int64_t(st) : b;
+}
+
+int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_chunk, int32_t chunk_len,
+                            const void* sink_k, const void* sink_v, int32_t sink_len, const void* ring_k,
+                            const void* ring_v, int32_t ring_slots, int64_t hist_len, int64_t window,
+                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float softmax_scale,
+                            void* out, int32_t out_dtype, float* lse_out, int32_t num_splits, void* workspace,
+                            int64_t workspace_bytes, void* stream) {
+  Shape sh;
+  int st = check_attn_shape(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads, head_dim,
+                            num_splits, &sh);
+  if (st != VICO_OK) return st;
+  if (out_dtype != VICO_DTYPE_BF16 && out_dtype != VICO_DTYPE_F32) return VICO_ERR_UNSUPPORTED;
+  if (isnan(softmax_scale) || isinf(softmax_scale)) return VICO_ERR_INVALID_ARG;
+  if (workspace_bytes < 0) return VICO_ERR_INVALID_ARG;
+  if (chunk_len == 0) return VICO_OK;
+  if (!q || !k_chunk || !v_chunk || !out) return VICO_ERR_INVALID_ARG;
+  if (sh.S > 0 && (!sink_k || !sink_v)) return VICO_ERR_INVALID_ARG;
+  if (sh.Wv > 0 && (!ring_k || !ring_v)) return VICO_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v, out, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return VICO_ERR_MISALIGNED;
+  if (lse_out && (reinterpret_cast<uintptr_t>(lse_out) & 3u)) return VICO_ERR_MISALIGNED;
+  if (sh.ws_bytes > 0 && (!workspace || workspace_bytes < sh.ws_bytes)) return VICO_ERR_WORKSPACE;
+  // The outputs must not alias any input.
+  const int64_t ob = int64_t(chunk_len) * num_q_heads * head_dim * (out_dtype == VICO_DTYPE_F32 ? 4 : 2);
+  const int64_t qb = int64_t(chunk_len) * num_q_heads * head_dim * 2;
+  const int64_t cb = int64_t(chunk_len) * num_kv_heads * head_dim * 2;
+  const int64_t sb = int64_t(sink_len) * num_kv_heads * head_dim * 2;
+  const int64_t rb = int64_t(ring_slots) * num_kv_heads * head_dim * 2;
+  const int64_t lb = lse_out ? int64_t(num_q_heads) * chunk_len * 4 : 0;
+  const void* ins[] = {q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v};
+  const int64_t inb[] = {qb, cb, cb, sb, sb, sh.Wv ? rb : 0, sh.Wv ? rb : 0};
+  for (int i = 0; i < 7; ++i)
+    if (ins[i] && (overlaps(out, ob, ins[i], inb[i]) || overlaps(lse_out, lb, ins[i], inb[i])))
+      return VICO_ERR_INVALID_ARG;
+  if (overlaps(out, ob, lse_out, lb)) return VICO_ERR_INVALID_ARG;
+
+  vico::AttnArgs a{};
+  a.q = (const uint16_t*)q;
+  a.kc = (const uint16_t*)k_chunk;
+  a.vc = (const uint16_t*)v_chunk;
+  a.sink_k = (const uint16_t*)sink_k;
+  a.sink_v = (const uint16_t*)sink_v;
+  a.ring_k = (const uint16_t*)ring_k;
+  a.ring_v = (const uint16_t*)ring_v;
+  a.out = out;
+  a.lse = lse_out;
+  if (sh.splits > 1) {
+    a.ws_o = (float*)workspace;
+    a.ws_lse = (float*)((char*)workspace + align256(int64_t(4) * sh.splits * sh.Hq * sh.C * sh.D));
+  }
+  a.C = sh.C; a.S = sh.S; a.R = sh.R; a.Wv = sh.Wv; a.ws = sh.ws;
+  a.Hq = sh.Hq; a.Hkv = sh.Hkv; a.D = sh.D;
+  a.splits = sh.splits;
+  a.out_f32 = out_dtype == VICO_DTYPE_F32;
+  const double scale = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(head_dim));
+  a.scale_log2 = (float)(scale * 1.4426950408889634);
+  const hipError_t e = vico::launch_attention(a, (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+int vico_kv_append(const void* k_chunk, const void* v_chunk, int32_t chunk_len, void* ring_k, void* ring_v,
+                   int32_t ring_slots, int64_t hist_len, int32_t num_kv_heads, int32_t head_dim, void* stream) {
+  if (chunk_len < 0 || ring_slots < 0 || hist_len < 0 || num_kv_heads < 1 || num_kv_heads > kMaxHeads)
+    return VICO_ERR_INVALID_ARG;
+  if (head_dim != 64 && head_dim != 128) return VICO_ERR_UNSUPPORTED;
+  if (chunk_len > ring_slots) return VICO_ERR_CAPACITY;
+  if (chunk_len == 0) return VICO_OK;
+  if (!k_chunk || !v_chunk || !ring_k || !ring_v) return VICO_ERR_INVALID_ARG;
+  const void* ptrs[] = {k_chunk, v_chunk, ring_k, ring_v};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return VICO_ERR_MISALIGNED;
+  const int64_t row = int64_t(num_kv_heads) * head_dim * 2;
+  const int64_t cb = row * chunk_len, rb = row * ring_slots;
+  if (overlaps(ring_k, rb, ring_v, rb) || overlaps(ring_k, rb, k_chunk, cb) || overlaps(ring_k, rb, v_chunk, cb) ||
+      overlaps(ring_v, rb, k_chunk, cb) || overlaps(ring_v, rb, v_chunk, cb))
+    return VICO_ERR_INVALID_ARG;
+  vico::AppendArgs a{};
+  a.kc = (const uint16_t*)k_chunk;
+  a.vc = (const uint16_t*)v_chunk;
+  a.rk = (uint16_t*)ring_k;
+  a.rv = (uint16_t*)ring_v;
+  a.C = chunk_len;
+  a.R = ring_slots;
+  a.p0 = (int)(hist_len % ring_slots);
+  a.row_elems = num_kv_heads * head_dim;
+  const hipError_t e = vico::launch_append(a, (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+}  // extern "C"

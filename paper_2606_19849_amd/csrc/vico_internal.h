@@ -1,0 +1,54 @@
+// Internal declarations shared by the HIP sources of libvico (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vico {
+
+// Tile geometry of the attention kernel.  A work-group of 4 waves owns
+// kBlockM = 128 query rows of one query head; each wave owns 32 rows.
+// Keys are walked in tiles of 8192 / head_dim keys so that a K tile plus a
+// V tile always take 32 KiB of LDS (double-buffered: 2 work-groups per CU
+// fit in the 160 KiB of LDS).
+constexpr int kBlockM = 128;
+constexpr int kThreads = 256;
+constexpr int kNumCUs = 256;        // MI355X: 8 XCDs x 32 CUs
+constexpr int kWgPerCU = 2;
+constexpr int kMaxSplits = 16;
+
+inline int key_tile(int head_dim) { return 8192 / head_dim; }
+
+// Everything the attention kernels need, resolved on the host.
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  const uint16_t* sink_k;
+  const uint16_t* sink_v;
+  const uint16_t* ring_k;
+  const uint16_t* ring_v;
+  void* out;
+  float* lse;          // may be null
+  float* ws_o;         // [splits][Hq][C][D] fp32, null when splits == 1
+  float* ws_lse;       // [splits][Hq][C] fp32 (log2 units)
+  int C, S, R, Wv, ws; // ws = first window slot = (H - Wv) mod R
+  int Hq, Hkv, D;
+  int splits;
+  int out_f32;
+  float scale_log2;    // softmax scale * log2(e)
+};
+
+struct AppendArgs {
+  const uint16_t* kc;
+  const uint16_t* vc;
+  uint16_t* rk;
+  uint16_t* rv;
+  int C, R, p0;        // p0 = hist_len mod R
+  int row_elems;       // Hkv * D
+};
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
+
+}  // namespace vico

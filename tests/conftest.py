@@ -28,3 +28,11 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+def pytest_runtest_logstart(nodeid, location):
+    # Name each GPU case on the real stderr before it runs, so that a run that
+    # ends abruptly still says which case it was in.
+    if "gpu" in nodeid or "test_gpu" in location[0]:
+        sys.__stderr__.write(f"[start] {nodeid}\n")
+        sys.__stderr__.flush()

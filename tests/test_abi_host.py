@@ -1,0 +1,143 @@
+"""Host-side checks of the C ABI: the library loads, exports every function the
+header declares, plans launches, and rejects bad arguments before any HIP call.
+None of these tests touches a GPU."""
+import ctypes
+
+import pytest
+
+import paper_2606_19849_amd as vico
+from synth import CONFIGS
+
+lib = vico.load_library()
+A = 0x10000          # fake, 16-byte aligned "device" addresses: validation never dereferences them
+B = 0x20000000
+MIS = 0x10008
+
+EXPECTED = {"vico_kv_append", "vico_chunk_prefill_attn", "vico_attn_plan", "vico_attn_workspace_bytes",
+            "vico_status_str", "vico_last_hip_error"}
+
+
+def test_header_declares_the_expected_entry_points():
+    assert set(vico.header_functions()) == EXPECTED
+
+
+@pytest.mark.parametrize("name", sorted(EXPECTED))
+def test_library_exports_every_header_symbol(name):
+    assert hasattr(lib, name)
+
+
+def test_single_hip_runtime_in_process():
+    """libvico resolves libamdhip64 to the copy torch already loaded."""
+    paths = set()
+    for line in open("/proc/self/maps"):
+        if "libamdhip64" in line:
+            paths.add(line.split()[-1])
+    assert len(paths) == 1, paths
+
+
+def test_status_strings():
+    for s in range(-6, 1):
+        assert lib.vico_status_str(s) and lib.vico_status_str(s) != b"unknown status"
+    assert lib.vico_status_str(-99) == b"unknown status"
+    assert lib.vico_last_hip_error() == 0
+
+
+def _attn(**kw):
+    a = dict(q=A, kc=A + 0x100000, vc=A + 0x200000, C=64, sk=A + 0x300000, sv=A + 0x400000, S=16,
+             rk=A + 0x500000, rv=A + 0x600000, R=256, H=456, W=256, Hq=2, Hkv=1, D=64, scale=0.0,
+             out=B, odt=1, lse=None, splits=0, ws=None, wsb=0, stream=None)
+    a.update(kw)
+    return lib.vico_chunk_prefill_attn(a["q"], a["kc"], a["vc"], a["C"], a["sk"], a["sv"], a["S"], a["rk"],
+                                       a["rv"], a["R"], a["H"], a["W"], a["Hq"], a["Hkv"], a["D"], a["scale"],
+                                       a["out"], a["odt"], a["lse"], a["splits"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Hq=3, Hkv=2), -1),                 # heads not grouped evenly
+    (dict(Hkv=0), -1),
+    (dict(D=96), -2),                        # unsupported head_dim
+    (dict(W=-2), -1),
+    (dict(C=-1), -1),
+    (dict(S=-1), -1),
+    (dict(H=-5), -1),
+    (dict(R=128), -3),                       # window 256 does not fit a 128-slot ring
+    (dict(W=-1, H=300), -3),                 # full history already partly evicted
+    (dict(q=None), -1),
+    (dict(out=None), -1),
+    (dict(sk=None), -1),                     # sink pointers required when S > 0
+    (dict(rk=None), -1),                     # ring pointers required when Wv > 0
+    (dict(q=MIS), -4),
+    (dict(out=B + 4), -4),
+    (dict(lse=B + 0x100002), -4),
+    (dict(odt=7), -2),
+    (dict(scale=float("nan")), -1),
+    (dict(splits=-1), -1),
+    (dict(out=A + 8 * 16), -1),              # output aliases q
+    (dict(lse=A + 0x500000 + 64), -1),       # lse aliases the ring
+    (dict(C=1 << 21), -1),                   # chunk beyond the supported maximum
+])
+def test_attention_rejects_bad_arguments(kw, status):
+    assert _attn(**kw) == status
+
+
+def test_attention_accepts_null_ring_when_no_history_is_visible():
+    # window 0 and no sink: nothing to validate on the ring side; C == 0 returns before launching
+    assert _attn(C=0, rk=None, rv=None, W=0, S=0, sk=None, sv=None) == 0
+
+
+def test_empty_chunk_is_a_noop():
+    assert _attn(C=0, q=None, kc=None, vc=None, out=None) == 0
+    assert lib.vico_kv_append(None, None, 0, None, None, 16, 5, 1, 64, None) == 0
+
+
+def test_split_workspace_is_required():
+    # 3B shape plans 4 splits and needs a workspace
+    sh = CONFIGS["3b"]
+    ns, wb = vico.vico_attn_plan(sh.chunk_len, sh.sink_len, sh.ring_slots, sh.hist_len, sh.window,
+                                 sh.num_q_heads, sh.num_kv_heads, sh.head_dim)
+    assert ns > 1 and wb > 0
+    assert _attn(C=sh.chunk_len, S=sh.sink_len, R=sh.ring_slots, H=sh.hist_len, W=sh.window, Hq=16, Hkv=2,
+                 D=128, q=A, kc=A + (1 << 26), vc=A + (2 << 26), sk=A + (3 << 26), sv=A + (4 << 26),
+                 rk=A + (5 << 26), rv=A + (6 << 26), out=B, ws=None, wsb=0) == -5
+    assert _attn(C=sh.chunk_len, S=sh.sink_len, R=sh.ring_slots, H=sh.hist_len, W=sh.window, Hq=16, Hkv=2,
+                 D=128, q=A, kc=A + (1 << 26), vc=A + (2 << 26), sk=A + (3 << 26), sv=A + (4 << 26),
+                 rk=A + (5 << 26), rv=A + (6 << 26), out=B, ws=B + (1 << 30), wsb=wb - 1) == -5
+
+
+@pytest.mark.parametrize("cfg,splits", [("tiny", 1), ("tiny_partial", 1), ("3b", 4), ("3b_wrap", 4), ("7b", 1),
+                                        ("7b_wrap", 1), ("full", 2), ("full_bounded", 2)])
+def test_plan_for_the_workloads(cfg, splits):
+    sh = CONFIGS[cfg]
+    ns, wb = vico.vico_attn_plan(sh.chunk_len, sh.sink_len, sh.ring_slots, sh.hist_len, sh.window,
+                                 sh.num_q_heads, sh.num_kv_heads, sh.head_dim)
+    assert ns == splits
+    if ns == 1:
+        assert wb == 0
+    else:
+        C, Hq, D = sh.chunk_len, sh.num_q_heads, sh.head_dim
+        o_bytes = (4 * ns * Hq * C * D + 255) // 256 * 256
+        assert wb == o_bytes + 4 * ns * Hq * C
+    assert vico.vico_attn_workspace_bytes(sh.chunk_len, sh.sink_len, sh.ring_slots, sh.hist_len, sh.window,
+                                          sh.num_q_heads, sh.num_kv_heads, sh.head_dim) == wb
+
+
+def test_forced_splits_are_clamped_to_the_key_tiles():
+    # 16 + 256 + 64 keys in tiles of 128 keys (head_dim 64) -> at most 3 splits
+    assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=8)[0] == 3
+    assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=2)[0] == 2
+    with pytest.raises(vico.VicoError):
+        vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=-3)
+
+
+@pytest.mark.parametrize("args,status", [
+    ((A, A + 0x1000, 17, B, B + 0x100000, 16, 0, 1, 64), -3),     # chunk longer than the ring
+    ((A, A + 0x1000, 4, B, B + 0x100000, 16, -1, 1, 64), -1),
+    ((A, A + 0x1000, 4, B, B + 0x100000, 16, 0, 1, 80), -2),
+    ((A, A + 0x1000, 4, B, B + 0x100000, 16, 0, 0, 64), -1),
+    ((MIS, A + 0x1000, 4, B, B + 0x100000, 16, 0, 1, 64), -4),
+    ((A, A + 0x1000, 4, None, B + 0x100000, 16, 0, 1, 64), -1),
+    ((A, A + 0x1000, 4, B, B + 64, 16, 0, 1, 64), -1),             # ring_k and ring_v overlap
+    ((B + 128, A + 0x1000, 4, B, B + 0x100000, 16, 0, 1, 64), -1),  # chunk inside the ring
+])
+def test_append_rejects_bad_arguments(args, status):
+    assert lib.vico_kv_append(*args, None) == status
