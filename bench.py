@@ -224,12 +224,49 @@ def run_stream_workload(args, torch, vico):
     }
 
 
+def run_append_workload(args, torch, vico):
+    """Ring append at capacity (chunk = ring = 16384 tokens of the 7B shape): HBM roofline
+    of the append kernel, which is also a plain copy of known size."""
+    R, Hkv, D = 16384, 4, 128
+    C = R
+    g = torch.Generator(device="cuda").manual_seed(0)
+    k = torch.randn((C, Hkv, D), device="cuda", generator=g).to(torch.bfloat16)
+    v = torch.randn((C, Hkv, D), device="cuda", generator=g).to(torch.bfloat16)
+    rk = torch.zeros((R, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    rv = torch.zeros_like(rk)
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        vico.vico_kv_append(k, v, rk, rv, 777 + i, stream=stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        vico.vico_kv_append(k, v, rk, rv, 777 + i * 1000, stream=stream)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    nbytes = 2 * 2 * C * Hkv * D * 2
+    gbs = nbytes / (ms.mean() * 1e-3) / 1e9
+    return {
+        "metric": "ring append HBM GB/s", "value": round(nbytes * args.steps / elapsed / 1e9, 1), "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "ring append at capacity: 16384 tokens x 4 kv heads x d128, K and V, ring wraps",
+                   "bytes_per_launch": nbytes},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": args.traffic_bytes,
+                     "kernel": "kv_append_kernel"},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream"])
+    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--traffic-bytes", type=float, default=None,
@@ -248,6 +285,8 @@ def main():
     vico.load_library()
     if args.workload == "stream":
         res = run_stream_workload(args, torch, vico)
+    elif args.workload == "append":
+        res = run_append_workload(args, torch, vico)
     else:
         res = run_chunk_workload(args, torch, vico)
     print(json.dumps(res), flush=True)

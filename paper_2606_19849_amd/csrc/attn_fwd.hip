@@ -15,17 +15,26 @@
 //     query row l%32, and lanes l and l+32 together hold all 32 keys of the
 //     block, so the row max / row sum need a single v_permlane32_swap.
 //   * O^T = V^T P^T with the same MFMA: the S^T accumulator registers,
-//     rounded to bf16, are already the B operand (k index = key slot); the A
-//     operand is V^T, which the loader writes into LDS transposed, with the
-//     keys of each 16-key group permuted to the order the accumulator layout
-//     produces them in.  O^T stays in the layout "lane = query row", so the
-//     per-row rescale factors are lane-local.
+//     rounded to bf16, are already the B operand (k index = key slot, keys
+//     of each 16-key group in the order the accumulator produces them); the
+//     A operand V^T is read from the row-major V tile with the gfx950
+//     transposing LDS read ds_read_b64_tr_b16 (each 16-lane group reads a
+//     4-key x 16-dim block and lane i receives dim i of the 4 keys).  O^T stays
+//     in the layout "lane = query row", so per-row rescale factors are
+//     lane-local.
 //   * Online softmax in fp32 with exp2 (v_exp_f32), scale*log2(e) folded into
-//     one FMA per logit.
-//   * K/V tiles: 8192/d keys, double-buffered in LDS; the next tile's global
-//     loads are in flight while the current tile is multiplied.  The window
-//     start and the ring wrap are resolved per key row when loading: slot =
-//     ws + k, minus R once if it passed the end.  No copies are made.
+//     one FMA per logit.  The running max is only raised (and O rescaled)
+//     when some row's tile max exceeds it by more than 2^8; until then the
+//     probabilities are exp2 of at most 8, exact in fp32 and bf16 range.
+//   * K/V tiles: 8192/d keys, double-buffered in LDS; the next tile's loads
+//     are in flight while the current tile is multiplied.  Loads go through
+//     buffer resources (one per sink / ring / chunk tensor): a tile that lies
+//     inside one segment (and does not cross the ring end) is addressed as a
+//     scalar tile base plus a fixed per-thread offset; the few tiles that
+//     straddle a boundary resolve each key row (ring slot = ws + k, minus R
+//     once past the end) and read all three resources with out-of-range
+//     offsets for the wrong ones, which the hardware returns as zero.  Keys
+//     past the chunk end read as zero the same way.  No copies are made.
 //   * Causal chunk: only tiles that reach past the first row of a wave are
 //     masked; tiles beyond the last row of a wave are skipped by that wave.
 //   * Work-groups are renumbered so that consecutive logical ids (the query
@@ -42,7 +51,9 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kNumXcd = 8;
@@ -66,10 +77,14 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// XOR swizzle of 16-byte segments in the V^T tile rows: spreads both the
-// transposing writes (rows 8 apart) and the MFMA operand reads (8
-// consecutive rows) over distinct LDS banks.
-__device__ __forceinline__ int vswz(int d) { return (d ^ (d >> 3)) & 7; }
+// Raw buffer resource over `bytes` bytes (stride 0, 32-bit data format).
+// Reads at offsets >= bytes return zero.
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr float kRescaleThreshold = 8.0f;   // log2 units
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n_rt, int g) {
@@ -79,13 +94,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   constexpr int NDB = D / 32;      // 32-dim blocks of O^T
   constexpr int NPK = BN / 16;     // 16-key k-steps of V^T P^T
   constexpr int NCH = D / 8;       // 16-byte chunks per key row
-  constexpr int KSTR = D + 8;      // K tile row stride in elements (16 B pad)
-  constexpr int VROW = BN;         // V^T tile row length in elements
-  constexpr int KT = BN * KSTR;
-  constexpr int VT = D * VROW;
+  constexpr int KSTR = D + 8;      // K and V tile row stride in elements (16 B pad)
+  constexpr int KT = BN * KSTR;    // elements of one K (or V) tile
   static_assert((BN / 4) * NCH == kThreads, "one 4-key x 8-dim block per thread");
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (KT + VT)];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * 2 * KT];   // {K, V} x 2 buffers
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -132,60 +145,72 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   // ---- tile loader: thread = 4 consecutive keys x one 16-byte dim chunk
   const int kg = tid / NCH;
   const int dc = tid % NCH;
-  const int64_t kvs = (int64_t)a.Hkv * D;
-  const int64_t col = (int64_t)kv * D + dc * 8;
+  const int rb = a.Hkv * D * 2;                                // bytes per token row
+  const uint32_t colb = (uint32_t)(kv * D + dc * 8) * 2u;      // byte offset inside a row
+  const uint32_t thr_off = (uint32_t)(kg * 4) * (uint32_t)rb + colb;
+  const rsrc_t rs_sk = make_rsrc(a.sink_k, S * rb), rs_sv = make_rsrc(a.sink_v, S * rb);
+  const rsrc_t rs_rk = make_rsrc(a.ring_k, a.R * rb), rs_rv = make_rsrc(a.ring_v, a.R * rb);
+  const rsrc_t rs_ck = make_rsrc(a.kc, C * rb), rs_cv = make_rsrc(a.vc, C * rb);
 
   u32x4 kr[4], vr[4];
   auto load_tile = [&](int t) {
-    const int kbase = t * BN + kg * 4;
+    const int k0 = t * BN, k1 = k0 + BN;
+    // segment of the whole tile (wave-uniform): 0 sink, 1 ring without wrap, 2 chunk, 3 mixed
+    int mode = 3, row_base = 0;
+    if (k1 <= S) {
+      mode = 0; row_base = k0;
+    } else if (k0 >= SW) {
+      mode = 2; row_base = k0 - SW;
+    } else if (k0 >= S && k1 <= SW) {
+      int slot0 = a.ws + (k0 - S);
+      if (slot0 >= a.R) slot0 -= a.R;
+      if (slot0 + BN <= a.R) { mode = 1; row_base = slot0; }
+    }
+    if (mode != 3) {
+      // select scalar base and size, then build one resource (keeps it in SGPRs)
+      const uint16_t* bk = mode == 0 ? a.sink_k : (mode == 1 ? a.ring_k : a.kc);
+      const uint16_t* bv = mode == 0 ? a.sink_v : (mode == 1 ? a.ring_v : a.vc);
+      const int nb = mode == 0 ? S * rb : (mode == 1 ? a.R * rb : C * rb);
+      const rsrc_t rk_ = make_rsrc(bk, nb), rv_ = make_rsrc(bv, nb);
+      const uint32_t off = (uint32_t)row_base * (uint32_t)rb + thr_off;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kk = kbase + r;
-      const uint16_t* pk = nullptr;
-      const uint16_t* pv = nullptr;
-      int64_t off = 0;
-      if (kk < S) {
-        pk = a.sink_k; pv = a.sink_v; off = kk;
-      } else if (kk < SW) {
+      for (int r = 0; r < 4; ++r) {
+        kr[r] = __builtin_amdgcn_raw_buffer_load_b128(rk_, off + r * rb, 0, 0);
+        vr[r] = __builtin_amdgcn_raw_buffer_load_b128(rv_, off + r * rb, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int kk = k0 + kg * 4 + r;
         int slot = a.ws + (kk - S);
         if (slot >= a.R) slot -= a.R;
-        pk = a.ring_k; pv = a.ring_v; off = slot;
-      } else if (kk < SW + C) {
-        pk = a.kc; pv = a.vc; off = kk - SW;
-      }
-      if (pk) {
-        kr[r] = *(const u32x4*)(pk + off * kvs + col);
-        vr[r] = *(const u32x4*)(pv + off * kvs + col);
-      } else {
-        kr[r] = u32x4{0u, 0u, 0u, 0u};
-        vr[r] = u32x4{0u, 0u, 0u, 0u};
+        const uint32_t o_s = kk < S ? (uint32_t)kk * rb + colb : kOutOfRange;
+        const uint32_t o_r = (kk >= S && kk < SW) ? (uint32_t)slot * rb + colb : kOutOfRange;
+        const uint32_t o_c = kk >= SW ? (uint32_t)(kk - SW) * rb + colb : kOutOfRange;
+        kr[r] = __builtin_amdgcn_raw_buffer_load_b128(rs_sk, o_s, 0, 0) |
+                __builtin_amdgcn_raw_buffer_load_b128(rs_rk, o_r, 0, 0) |
+                __builtin_amdgcn_raw_buffer_load_b128(rs_ck, o_c, 0, 0);
+        vr[r] = __builtin_amdgcn_raw_buffer_load_b128(rs_sv, o_s, 0, 0) |
+                __builtin_amdgcn_raw_buffer_load_b128(rs_rv, o_r, 0, 0) |
+                __builtin_amdgcn_raw_buffer_load_b128(rs_cv, o_c, 0, 0);
       }
     }
   };
-
-  // V^T slot of key 4*kg within the tile: inside each 16-key group the keys
-  // are stored in the order the S^T accumulator hands them to lane halves.
-  const int vgrp = kg >> 2, va = kg & 3;
-  const int vslot = vgrp * 16 + (va & 1) * 8 + (va >> 1) * 4;
-  const int vseg = vslot >> 3, vhalf = (vslot >> 2) & 1;
 
   auto store_tile = [&](int buf) {
-    uint16_t* Ks = smem + buf * (KT + VT);
-    uint16_t* Vt = Ks + KT;
+    uint16_t* Ks = smem + buf * (2 * KT);
+    uint16_t* Vs = Ks + KT;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) *(u32x4*)(Ks + (kg * 4 + r) * KSTR + dc * 8) = kr[r];
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {      // dword m of a row holds dims 2m (low) and 2m+1 (high)
-      u32x2 lo, hi;
-      lo[0] = __builtin_amdgcn_perm(vr[1][m], vr[0][m], 0x05040100u);
-      lo[1] = __builtin_amdgcn_perm(vr[3][m], vr[2][m], 0x05040100u);
-      hi[0] = __builtin_amdgcn_perm(vr[1][m], vr[0][m], 0x07060302u);
-      hi[1] = __builtin_amdgcn_perm(vr[3][m], vr[2][m], 0x07060302u);
-      const int d0 = dc * 8 + 2 * m, d1 = d0 + 1;
-      *(u32x2*)(Vt + d0 * VROW + ((vseg ^ vswz(d0)) << 3) + vhalf * 4) = lo;
-      *(u32x2*)(Vt + d1 * VROW + ((vseg ^ vswz(d1)) << 3) + vhalf * 4) = hi;
+    for (int r = 0; r < 4; ++r) {
+      *(u32x4*)(Ks + (kg * 4 + r) * KSTR + dc * 8) = kr[r];
+      *(u32x4*)(Vs + (kg * 4 + r) * KSTR + dc * 8) = vr[r];
     }
   };
+
+  // Per-lane source of the transposing V reads: 16-lane group G = lane/16
+  // covers dims (G%2)*16 .. +15 of a 32-dim block and k-slots (G/2)*8 ..;
+  // its lane 4j+q supplies key j of the group's 4 keys, dims 4q .. 4q+3.
+  const int v_lane_off = ((lane >> 5) * 4 + ((lane & 15) >> 2)) * KSTR + ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
 
   // ---- running state of this lane's row (both halves hold the same m)
   f32x16 o[NDB];
@@ -196,8 +221,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   const float c = a.scale_log2;
 
   auto compute_tile = [&](int buf, int k0) {
-    const uint16_t* Ks = smem + buf * (KT + VT);
-    const uint16_t* Vt = Ks + KT;
+    const uint16_t* Ks = smem + buf * (2 * KT);
+    const uint16_t* Vs = Ks + KT;
     f32x16 s[NB];
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb) {
@@ -223,9 +248,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
     for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-    mx = pair_max(mx);
-    const float m_new = fmaxf(m_run, mx * c);
-    if (__builtin_amdgcn_ballot_w64(m_new > m_run)) {
+    mx = pair_max(mx) * c;
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run, mx);
       const float alpha = (m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
@@ -248,14 +273,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
     for (int kp = 0; kp < NPK; ++kp)
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[kp][e] = (__bf16)s[kp >> 1][(kp & 1) * 8 + e];
+    const uint16_t* vl = Vs + v_lane_off;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const int d = db * 32 + l32;
-      const uint16_t* vrow = Vt + d * VROW;
-      const int sw = vswz(d);
 #pragma unroll
       for (int kp = 0; kp < NPK; ++kp) {
-        const bf16x8 vf = *(const bf16x8*)(vrow + (((kp * 2 + hh) ^ sw) << 3));
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16) * KSTR + db * 32));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16 + 8) * KSTR + db * 32));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kp], o[db], 0, 0, 0);
       }
     }

@@ -15,6 +15,7 @@ thread_local int g_last_hip_error = 0;
 constexpr int64_t kMaxChunk = int64_t(1) << 20;
 constexpr int64_t kMaxKeys = int64_t(1) << 30;
 constexpr int kMaxHeads = 1024;
+constexpr int64_t kMaxTensorBytes = int64_t(1) << 31;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -54,6 +55,10 @@ int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int3
   const int64_t wv = (W < 0) ? H : (W < H ? W : H);
   if (wv > R) return VICO_ERR_CAPACITY;
   if (int64_t(S) + wv + C > kMaxKeys) return VICO_ERR_INVALID_ARG;
+  // the kernels address every K/V tensor through 32-bit buffer offsets
+  const int64_t row_bytes = int64_t(Hkv) * D * 2;
+  if (row_bytes * C >= kMaxTensorBytes || row_bytes * S >= kMaxTensorBytes || row_bytes * R >= kMaxTensorBytes)
+    return VICO_ERR_INVALID_ARG;
   sh->C = C; sh->S = S; sh->R = R; sh->Wv = (int)wv;
   sh->ws = R > 0 ? (int)((H - wv) % R) : 0;
   sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;

@@ -88,15 +88,20 @@ def test_large_logits_stay_finite():
 
 
 def test_split_counts_agree():
-    """Every split count gives the same result up to rounding."""
+    """Every split count meets the oracle tolerance; results differ between split
+    counts only by where the bf16 probabilities are rounded (each split keeps its
+    own running max), so two of them agree within twice the per-result bound."""
     sh = SMALL["auto_split"]
     inp = make_chunk_inputs(sh, seed=106, family="F2")
     dc = DeviceChunk(inp)
+    ref, ref_lse = oracle_result(inp)
     base, base_lse = dc.attention(torch.float32, num_splits=1)
+    check_f32(base, ref, base_lse, ref_lse)
     for ns in (2, 4, 7, 16):
         o, lse = dc.attention(torch.float32, num_splits=ns)
-        assert np.max(np.abs(o - base)) <= 2e-3
-        assert np.max(np.abs(lse - base_lse)) <= 1e-4
+        check_f32(o, ref, lse, ref_lse)
+        assert np.max(np.abs(o - base)) <= 2e-2
+        assert np.max(np.abs(lse - base_lse)) <= 2e-3
 
 
 def _sample_rows(C, n=40, seed=0):
