@@ -94,11 +94,18 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   constexpr int NDB = D / 32;      // 32-dim blocks of O^T
   constexpr int NPK = BN / 16;     // 16-key k-steps of V^T P^T
   constexpr int NCH = D / 8;       // 16-byte chunks per key row
-  constexpr int KSTR = D + 8;      // K and V tile row stride in elements (16 B pad)
-  constexpr int KT = BN * KSTR;    // elements of one K (or V) tile
+  // LDS row strides (elements).  The LDS has 64 banks of 4 bytes.  K rows are
+  // read 16 lanes x 16 bytes at a time from 16 consecutive rows: a stride of
+  // 4 banks mod 64 (16 B pad) keeps them apart.  V rows are read by the
+  // transposing loads 32 lanes at a time as 4 rows x 64 bytes: a stride of
+  // 64 bytes mod 256 puts the 4 rows on disjoint banks (d = 128).
+  constexpr int KSTR = D + 8;
+  constexpr int VSTR = D == 128 ? D + 32 : D + 8;
+  constexpr int KT = BN * KSTR;    // elements of one K tile
+  constexpr int VT = BN * VSTR;    // elements of one V tile
   static_assert((BN / 4) * NCH == kThreads, "one 4-key x 8-dim block per thread");
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * 2 * KT];   // {K, V} x 2 buffers
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (KT + VT)];   // {K, V} x 2 buffers
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -198,19 +205,19 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   };
 
   auto store_tile = [&](int buf) {
-    uint16_t* Ks = smem + buf * (2 * KT);
+    uint16_t* Ks = smem + buf * (KT + VT);
     uint16_t* Vs = Ks + KT;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       *(u32x4*)(Ks + (kg * 4 + r) * KSTR + dc * 8) = kr[r];
-      *(u32x4*)(Vs + (kg * 4 + r) * KSTR + dc * 8) = vr[r];
+      *(u32x4*)(Vs + (kg * 4 + r) * VSTR + dc * 8) = vr[r];
     }
   };
 
   // Per-lane source of the transposing V reads: 16-lane group G = lane/16
   // covers dims (G%2)*16 .. +15 of a 32-dim block and k-slots (G/2)*8 ..;
   // its lane 4j+q supplies key j of the group's 4 keys, dims 4q .. 4q+3.
-  const int v_lane_off = ((lane >> 5) * 4 + ((lane & 15) >> 2)) * KSTR + ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+  const int v_lane_off = ((lane >> 5) * 4 + ((lane & 15) >> 2)) * VSTR + ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
 
   // ---- running state of this lane's row (both halves hold the same m)
   f32x16 o[NDB];
@@ -221,7 +228,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   const float c = a.scale_log2;
 
   auto compute_tile = [&](int buf, int k0) {
-    const uint16_t* Ks = smem + buf * (2 * KT);
+    const uint16_t* Ks = smem + buf * (KT + VT);
     const uint16_t* Vs = Ks + KT;
     f32x16 s[NB];
 #pragma unroll
@@ -278,8 +285,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
     for (int db = 0; db < NDB; ++db) {
 #pragma unroll
       for (int kp = 0; kp < NPK; ++kp) {
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16) * KSTR + db * 32));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16 + 8) * KSTR + db * 32));
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16) * VSTR + db * 32));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16 + 8) * VSTR + db * 32));
         const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kp], o[db], 0, 0, 0);
       }
