@@ -32,6 +32,26 @@ PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 
 PEAK_HBM_GBS = 8000.0
 
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SRC = {"attn_fwd_kernel<128>": "paper_2606_19849_amd/csrc/attn_fwd.hip",
+              "kv_append_kernel": "paper_2606_19849_amd/csrc/kv_append.hip"}
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 summary of this kernel and
+    workload, or None when there is none or the kernel source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = dict(line.split(":", 1) for line in open(path) if ":" in line and not line.startswith("#"))
+    fields = {k.strip(): v.strip() for k, v in fields.items()}
+    src = open(os.path.join(ROOT, KERNEL_SRC[kernel]), "rb").read()
+    if fields.get("kernel") != kernel or fields.get("kernel_source_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    return float(fields["hbm_bytes_per_launch"])
+
+
 def attn_flops(C, S, Wv, Hq, D, rows=None):
     """Algorithmic flops: 4*d per (query row, visible key) per head; masked pairs excluded."""
     r = np.arange(C) if rows is None else np.asarray(rows)
@@ -154,7 +174,9 @@ def run_chunk_workload(args, torch, vico):
         "append_GBps": round(app_bytes / (app_ms.mean() * 1e-3) / 1e9, 1) if not full else None,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": args.traffic_bytes, "kernel": "attn_fwd_kernel<128>",
+                     "traffic": args.traffic_bytes if args.traffic_bytes is not None
+                     else measured_traffic("attn_fwd_kernel<128>", args.workload),
+                     "kernel": "attn_fwd_kernel<128>",
                      "flops_per_launch": fl},
     }
     if not args.no_cpu_baseline:
@@ -256,7 +278,9 @@ def run_append_workload(args, torch, vico):
         "config": {"workload": "ring append at capacity: 16384 tokens x 4 kv heads x d128, K and V, ring wraps",
                    "bytes_per_launch": nbytes},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": args.traffic_bytes,
+                     "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": args.traffic_bytes if args.traffic_bytes is not None
+                     else measured_traffic("kv_append_kernel", "append"),
                      "kernel": "kv_append_kernel"},
     }
 
