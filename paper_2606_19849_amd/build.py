@@ -46,6 +46,12 @@ def build(verbose: bool = False, extra_flags=()) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
+    # A kernel whose host-side launch stub was not emitted links into an
+    # unloadable library; refuse it here instead of at load time.
+    nm = subprocess.run(["nm", "-u", tmp], capture_output=True, text=True)
+    missing = [l.split()[-1] for l in nm.stdout.splitlines() if "__device_stub__" in l]
+    if missing:
+        raise RuntimeError(f"libvico.so references kernel stubs that were not emitted: {missing}")
     os.replace(tmp, LIB)
     return LIB
 

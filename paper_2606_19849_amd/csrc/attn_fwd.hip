@@ -7,8 +7,10 @@
 // at token granularity, causal inside the chunk).
 //
 // Mapping onto the hardware
-//   * Work-group = 4 waves = 128 query rows of one query head (one key range
-//     when split).  Each wave owns 32 rows for the whole key loop.
+//   * Work-group = 4 waves, one per SIMD (each wave may use the whole 512-entry
+//     register file), = 256 query rows of one query head (one key range when
+//     split).  Each wave owns 64 rows -- two 32-row MFMA blocks -- for the
+//     whole key loop, so every K and V fragment read from LDS feeds two MFMAs.
 //   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: the K tile (from LDS) is the
 //     A operand, the wave's Q rows (held in VGPRs for the whole loop) the B
 //     operand.  In the accumulator layout lane l then holds 16 logits of
@@ -26,7 +28,7 @@
 //     one FMA per logit.  The running max is only raised (and O rescaled)
 //     when some row's tile max exceeds it by more than 2^8; until then the
 //     probabilities are exp2 of at most 8, exact in fp32 and bf16 range.
-//   * K/V tiles: 8192/d keys, double-buffered in LDS; the next tile's loads
+//   * K/V tiles: 64 keys, double-buffered in LDS; the next tile's loads
 //     are in flight while the current tile is multiplied.  Loads go through
 //     buffer resources (one per sink / ring / chunk tensor): a tile that lies
 //     inside one segment (and does not cross the ring end) is addressed as a
@@ -35,12 +37,15 @@
 //     once past the end) and read all three resources with out-of-range
 //     offsets for the wrong ones, which the hardware returns as zero.  Keys
 //     past the chunk end read as zero the same way.  No copies are made.
-//   * Causal chunk: only tiles that reach past the first row of a wave are
-//     masked; tiles beyond the last row of a wave are skipped by that wave.
+//   * Causal chunk: only tiles that reach past the first row of a wave run the
+//     masked variant of the tile body; tiles beyond the last row of a wave are
+//     skipped by that wave.
 //   * Work-groups are renumbered so that consecutive logical ids (the query
 //     heads of one KV head) land on the same XCD and share its L2.
 //   * Optional split of the key range (for chunks too small to fill 256 CUs):
 //     each split writes fp32 O and log2-sum-exp; a merge kernel combines them.
+
+#include <type_traits>
 
 #include "vico_internal.h"
 
@@ -51,8 +56,10 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr float kLn2 = 0.6931471805599453f;
@@ -83,29 +90,53 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* p, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
 }
 
+// 16 bytes per lane from a buffer straight into LDS: lane i writes lds + 16*i.
+// Kept in a device-only function: used inline in a kernel body, the builtin
+// makes the host compilation pass drop the kernel's launch stub.
+__device__ __forceinline__ void load_lds16(rsrc_t r, lds_void* lds, uint32_t voffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voffset, 0, 0, 0);
+}
+
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n_rt, int g) {
-  constexpr int BN = 8192 / D;     // keys per tile
-  constexpr int NB = BN / 32;      // 32-key blocks of S^T per tile
-  constexpr int NKS = D / 16;      // k-steps of Q K^T
-  constexpr int NDB = D / 32;      // 32-dim blocks of O^T
-  constexpr int NPK = BN / 16;     // 16-key k-steps of V^T P^T
-  constexpr int NCH = D / 8;       // 16-byte chunks per key row
-  // LDS row strides (elements).  The LDS has 64 banks of 4 bytes.  K rows are
-  // read 16 lanes x 16 bytes at a time from 16 consecutive rows: a stride of
-  // 4 banks mod 64 (16 B pad) keeps them apart.  V rows are read by the
-  // transposing loads 32 lanes at a time as 4 rows x 64 bytes: a stride of
-  // 64 bytes mod 256 puts the 4 rows on disjoint banks (d = 128).
-  constexpr int KSTR = D + 8;
-  constexpr int VSTR = D == 128 ? D + 32 : D + 8;
-  constexpr int KT = BN * KSTR;    // elements of one K tile
-  constexpr int VT = BN * VSTR;    // elements of one V tile
-  static_assert((BN / 4) * NCH == kThreads, "one 4-key x 8-dim block per thread");
+  constexpr int BN = kKeyTile;         // keys per tile
+  constexpr int RB = kRowBlocks;       // 32-row blocks per wave
+  constexpr int BM = kBlockM;          // rows per work-group
+  constexpr int NKS = D / 16;          // k-steps of Q K^T
+  constexpr int NDB = D / 32;          // 32-dim blocks of O^T
+  // LDS tiles are dense rows of 2*D bytes (the direct loads below write each
+  // wave's 64 x 16 bytes contiguously), with 16-byte units permuted inside a
+  // row against bank conflicts; the LDS has 64 banks of 4 bytes:
+  //   K: unit u of row r sits at u ^ fk(r).  A K fragment read services 16
+  //      lanes = 16 consecutive rows at one unit; fk makes them distinct.
+  //   V: unit u of row r sits at u ^ fv(r).  A transposing read services 32
+  //      lanes = 4 consecutive rows x 4 units; fv spreads the rows apart.
+  constexpr int UPR = D / 8;           // 16-byte units per row
+  constexpr int RBY = D * 2;           // bytes per LDS row
+  constexpr int KT = BN * D;           // elements of one K (or V) tile
+  constexpr int VT = BN * D;
+  constexpr int NLD = BN * RBY / 1024 / 4;   // direct 1 KiB loads per wave per tile (K or V)
+  constexpr int RPL = 1024 / RBY;            // rows per direct load
+  static_assert(NLD * 4 * 1024 == BN * RBY, "direct loads cover the tile");
+  auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
+  auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (KT + VT)];   // {K, V} x 2 buffers
+  // Two K/V buffers (tile t in buffer t mod 2; the next tile loads while this
+  // one is multiplied).  Separate arrays let the compiler see that reads of
+  // one buffer do not wait for the direct loads landing in the other.
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds0[KT], k_lds1[KT];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds0[VT], v_lds1[VT];
+  auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
+    if constexpr (decltype(b)::value == 0) return k_lds0;
+    else return k_lds1;
+  };
+  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
+    if constexpr (decltype(b)::value == 0) return v_lds0;
+    else return v_lds1;
+  };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -124,230 +155,338 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   const int h = kv * g + qh;
 
   const int C = a.C, S = a.S, SW = a.S + a.Wv;
-  const int row0 = rt * kBlockM;
-  const int row_last = min(row0 + kBlockM, C) - 1;
+  const int row0 = rt * BM;
+  const int row_last = min(row0 + BM, C) - 1;
   const int n_tiles = (SW + row_last + 1 + BN - 1) / BN;
   const int t_lo = (int)((int64_t)n_tiles * sp / a.splits);
   const int t_hi = (int)((int64_t)n_tiles * (sp + 1) / a.splits);
 
-  const int wrow0 = row0 + wave * 32;
-  const int row = wrow0 + l32;
+  // this wave: rows wrow0 + rb*32 + l32, rb < RB
+  const int wrow0 = row0 + wave * 32 * RB;
   const bool wave_active = wrow0 < C;
-  const int row_c = min(row, C - 1);
-  const int key_lim = SW + row_c;                       // last key visible to this row
-  const int wave_first_lim = SW + min(wrow0, C - 1);    // ... to the wave's first row
-  const int wave_last_lim = SW + min(wrow0 + 31, C - 1);
+  const int wave_first_lim = SW + min(wrow0, C - 1);            // last key of the wave's first row
+  const int wave_last_lim = SW + min(wrow0 + 32 * RB - 1, C - 1);
+  int key_lim[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) key_lim[rb] = SW + min(wrow0 + rb * 32 + l32, C - 1);
 
   // ---- Q rows of this wave as MFMA B fragments (lane: row l32, dims hh*8..+8)
-  bf16x8 qf[NKS];
-  {
-    const uint16_t* qp = a.q + ((int64_t)row_c * a.Hq + h) * D + hh * 8;
+  bf16x8 qf[RB][NKS];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = wrow0 + rb * 32 + l32;
+    const uint16_t* qp = a.q + ((int64_t)min(row, C - 1) * a.Hq + h) * D + hh * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      u32x4 v = (row < C) ? *(const u32x4*)(qp + ks * 16) : u32x4{0u, 0u, 0u, 0u};
-      qf[ks] = __builtin_bit_cast(bf16x8, v);
+      const u32x4 v = (row < C) ? *(const u32x4*)(qp + ks * 16) : u32x4{0u, 0u, 0u, 0u};
+      qf[rb][ks] = __builtin_bit_cast(bf16x8, v);
     }
   }
 
-  // ---- tile loader: thread = 4 consecutive keys x one 16-byte dim chunk
-  const int kg = tid / NCH;
-  const int dc = tid % NCH;
-  const int rb = a.Hkv * D * 2;                                // bytes per token row
-  const uint32_t colb = (uint32_t)(kv * D + dc * 8) * 2u;      // byte offset inside a row
-  const uint32_t thr_off = (uint32_t)(kg * 4) * (uint32_t)rb + colb;
-  const rsrc_t rs_sk = make_rsrc(a.sink_k, S * rb), rs_sv = make_rsrc(a.sink_v, S * rb);
-  const rsrc_t rs_rk = make_rsrc(a.ring_k, a.R * rb), rs_rv = make_rsrc(a.ring_v, a.R * rb);
-  const rsrc_t rs_ck = make_rsrc(a.kc, C * rb), rs_cv = make_rsrc(a.vc, C * rb);
+  // ---- tile loader.  Direct load n of wave w fills LDS rows w*BN/4 + n*RPL ..
+  // (RPL rows): lane i writes unit i % UPR of row w*BN/4 + n*RPL + i / UPR and
+  // fetches the logical unit that belongs there under the swizzle.
+  const int rbytes = a.Hkv * D * 2;                            // bytes per token row in HBM
+  const rsrc_t rs_sk = make_rsrc(a.sink_k, S * rbytes), rs_sv = make_rsrc(a.sink_v, S * rbytes);
+  const rsrc_t rs_rk = make_rsrc(a.ring_k, a.R * rbytes), rs_rv = make_rsrc(a.ring_v, a.R * rbytes);
+  const rsrc_t rs_ck = make_rsrc(a.kc, C * rbytes), rs_cv = make_rsrc(a.vc, C * rbytes);
+  int ld_row[NLD];                // tile row filled by this lane in load n
+  uint32_t ld_ck[NLD], ld_cv[NLD];  // byte offset of the fetched K / V unit inside a token row
+#pragma unroll
+  for (int n = 0; n < NLD; ++n) {
+    const int r = wave * (BN / 4) + n * RPL + lane / UPR;
+    const int pu = lane % UPR;
+    ld_row[n] = r;
+    ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ fk(r)) * 16);
+    ld_cv[n] = (uint32_t)(kv * D * 2 + (pu ^ fv(r)) * 16);
+  }
 
-  u32x4 kr[4], vr[4];
-  auto load_tile = [&](int t) {
+  // tile kind (wave-uniform): 0 sink, 1 ring without wrap, 2 chunk, all rows
+  // inside the tensor; 3 anything else (segment boundary, ring end, chunk end)
+  auto tile_mode = [&](int t, int& row_base) __attribute__((always_inline)) {
     const int k0 = t * BN, k1 = k0 + BN;
-    // segment of the whole tile (wave-uniform): 0 sink, 1 ring without wrap, 2 chunk, 3 mixed
-    int mode = 3, row_base = 0;
-    if (k1 <= S) {
-      mode = 0; row_base = k0;
-    } else if (k0 >= SW) {
-      mode = 2; row_base = k0 - SW;
-    } else if (k0 >= S && k1 <= SW) {
+    row_base = 0;
+    if (k1 <= S) { row_base = k0; return 0; }
+    if (k0 >= SW && k1 <= SW + C) { row_base = k0 - SW; return 2; }
+    if (k0 >= S && k1 <= SW) {
       int slot0 = a.ws + (k0 - S);
       if (slot0 >= a.R) slot0 -= a.R;
-      if (slot0 + BN <= a.R) { mode = 1; row_base = slot0; }
+      if (slot0 + BN <= a.R) { row_base = slot0; return 1; }
     }
+    return 3;
+  };
+
+  // fast tiles: asynchronous direct loads into LDS buffer `buf`
+  auto load_tile_direct = [&](auto buf, int mode, int row_base) __attribute__((always_inline)) {
+    uint16_t* Ks = kbuf(buf);
+    uint16_t* Vs = vbuf(buf);
+    const uint16_t* bk = mode == 0 ? a.sink_k : (mode == 1 ? a.ring_k : a.kc);
+    const uint16_t* bv = mode == 0 ? a.sink_v : (mode == 1 ? a.ring_v : a.vc);
+    const int nb = mode == 0 ? S * rbytes : (mode == 1 ? a.R * rbytes : C * rbytes);
+    const rsrc_t rk_ = make_rsrc(bk, nb), rv_ = make_rsrc(bv, nb);
+#pragma unroll
+    for (int n = 0; n < NLD; ++n) {
+      const uint32_t rowoff = (uint32_t)(row_base + ld_row[n]) * (uint32_t)rbytes;
+      lds_void* kd = (lds_void*)(Ks + (wave * (BN / 4) + n * RPL) * D);
+      lds_void* vd = (lds_void*)(Vs + (wave * (BN / 4) + n * RPL) * D);
+      load_lds16(rk_, kd, rowoff + ld_ck[n]);
+      load_lds16(rv_, vd, rowoff + ld_cv[n]);
+    }
+  };
+
+  // other tiles: resolve each key row, read all three tensors (out-of-range
+  // offsets return zero), combine, and write the same LDS units.  Synchronous.
+  auto load_tile_rows = [&](auto buf, int t) __attribute__((always_inline)) {
+    uint16_t* Ks = kbuf(buf);
+    uint16_t* Vs = vbuf(buf);
+    const int k0 = t * BN;
+#pragma unroll
+    for (int n = 0; n < NLD; ++n) {
+      const int kk = k0 + ld_row[n];
+      int slot = a.ws + (kk - S);
+      if (slot >= a.R) slot -= a.R;
+      const uint32_t o_s = kk < S ? (uint32_t)kk * rbytes : kOutOfRange;
+      const uint32_t o_r = (kk >= S && kk < SW) ? (uint32_t)slot * rbytes : kOutOfRange;
+      const uint32_t o_c = kk >= SW ? (uint32_t)(kk - SW) * rbytes : kOutOfRange;
+      const u32x4 kx = __builtin_amdgcn_raw_buffer_load_b128(rs_sk, o_s + ld_ck[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_rk, o_r + ld_ck[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_ck, o_c + ld_ck[n], 0, 0);
+      const u32x4 vx = __builtin_amdgcn_raw_buffer_load_b128(rs_sv, o_s + ld_cv[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_rv, o_r + ld_cv[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_cv, o_c + ld_cv[n], 0, 0);
+      const int pos = ld_row[n] * D + (lane % UPR) * 8;
+      *(u32x4*)(Ks + pos) = kx;
+      *(u32x4*)(Vs + pos) = vx;
+    }
+  };
+
+  // returns true when the tile went out as asynchronous direct loads
+  auto load_tile = [&](auto buf, int t) __attribute__((always_inline)) {
+    int row_base;
+    const int mode = tile_mode(t, row_base);
     if (mode != 3) {
-      // select scalar base and size, then build one resource (keeps it in SGPRs)
-      const uint16_t* bk = mode == 0 ? a.sink_k : (mode == 1 ? a.ring_k : a.kc);
-      const uint16_t* bv = mode == 0 ? a.sink_v : (mode == 1 ? a.ring_v : a.vc);
-      const int nb = mode == 0 ? S * rb : (mode == 1 ? a.R * rb : C * rb);
-      const rsrc_t rk_ = make_rsrc(bk, nb), rv_ = make_rsrc(bv, nb);
-      const uint32_t off = (uint32_t)row_base * (uint32_t)rb + thr_off;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        kr[r] = __builtin_amdgcn_raw_buffer_load_b128(rk_, off + r * rb, 0, 0);
-        vr[r] = __builtin_amdgcn_raw_buffer_load_b128(rv_, off + r * rb, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kk = k0 + kg * 4 + r;
-        int slot = a.ws + (kk - S);
-        if (slot >= a.R) slot -= a.R;
-        const uint32_t o_s = kk < S ? (uint32_t)kk * rb + colb : kOutOfRange;
-        const uint32_t o_r = (kk >= S && kk < SW) ? (uint32_t)slot * rb + colb : kOutOfRange;
-        const uint32_t o_c = kk >= SW ? (uint32_t)(kk - SW) * rb + colb : kOutOfRange;
-        kr[r] = __builtin_amdgcn_raw_buffer_load_b128(rs_sk, o_s, 0, 0) |
-                __builtin_amdgcn_raw_buffer_load_b128(rs_rk, o_r, 0, 0) |
-                __builtin_amdgcn_raw_buffer_load_b128(rs_ck, o_c, 0, 0);
-        vr[r] = __builtin_amdgcn_raw_buffer_load_b128(rs_sv, o_s, 0, 0) |
-                __builtin_amdgcn_raw_buffer_load_b128(rs_rv, o_r, 0, 0) |
-                __builtin_amdgcn_raw_buffer_load_b128(rs_cv, o_c, 0, 0);
-      }
+      load_tile_direct(buf, mode, row_base);
+      return true;
     }
+    load_tile_rows(buf, t);
+    return false;
   };
 
-  auto store_tile = [&](int buf) {
-    uint16_t* Ks = smem + buf * (KT + VT);
-    uint16_t* Vs = Ks + KT;
+  // per-lane LDS byte offsets of the MFMA operand reads
+  //   K fragment (kb, ks): row kb*32 + l32, logical unit 2*ks + hh
+  uint32_t k_rd[NKS];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      *(u32x4*)(Ks + (kg * 4 + r) * KSTR + dc * 8) = kr[r];
-      *(u32x4*)(Vs + (kg * 4 + r) * VSTR + dc * 8) = vr[r];
-    }
-  };
-
-  // Per-lane source of the transposing V reads: 16-lane group G = lane/16
-  // covers dims (G%2)*16 .. +15 of a 32-dim block and k-slots (G/2)*8 ..;
-  // its lane 4j+q supplies key j of the group's 4 keys, dims 4q .. 4q+3.
-  const int v_lane_off = ((lane >> 5) * 4 + ((lane & 15) >> 2)) * VSTR + ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
-
-  // ---- running state of this lane's row (both halves hold the same m)
-  f32x16 o[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) o[db] = f32x16{};
-  float m_run = -INFINITY;
-  float l_run = 0.f;
-  const float c = a.scale_log2;
-
-  auto compute_tile = [&](int buf, int k0) {
-    const uint16_t* Ks = smem + buf * (KT + VT);
-    const uint16_t* Vs = Ks + KT;
-    f32x16 s[NB];
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb) {
-      s[kb] = f32x16{};
-      const uint16_t* kp = Ks + (kb * 32 + l32) * KSTR + hh * 8;
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const bf16x8 kf = *(const bf16x8*)(kp + ks * 16);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[kb], 0, 0, 0);
-      }
-    }
-    if (k0 + BN - 1 > wave_first_lim) {     // tile reaches into the causal part for this wave
-#pragma unroll
-      for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kk = k0 + kb * 32 + 8 * (v >> 2) + hh * 4 + (v & 3);
-          if (kk > key_lim) s[kb][v] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-    mx = pair_max(mx) * c;
-    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = (m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    float lsum = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][v], c, -m_use));
-        s[kb][v] = p;
-        lsum += p;
-      }
-    l_run += lsum;
-    bf16x8 pf[NPK];
-#pragma unroll
-    for (int kp = 0; kp < NPK; ++kp)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pf[kp][e] = (__bf16)s[kp >> 1][(kp & 1) * 8 + e];
-    const uint16_t* vl = Vs + v_lane_off;
+  for (int ks = 0; ks < NKS; ++ks) k_rd[ks] = (uint32_t)(l32 * RBY + (((2 * ks) | hh) ^ fk(l32)) * 16);
+  //   V^T fragment (db, kp, half): 16-lane group G = lane/16 covers dims
+  //   (G%2)*16 .. +15 of a 32-dim block and k-slots (G/2)*8 ..; its lane
+  //   4j+q supplies key j of the group's 4 keys (row kp*16 + half*8 +
+  //   (G/2)*4 + j), dims 4q .. 4q+3.
+  uint32_t v_rd[NDB];
+  {
+    const int j = (lane & 15) >> 2, q = lane & 3;
+    const int r = (lane >> 5) * 4 + j;            // row within the 8-row half-group (fv depends on r mod 4 only)
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
+      const int u = db * 4 + ((lane >> 4) & 1) * 2 + (q >> 1);
+      v_rd[db] = (uint32_t)(r * RBY + (u ^ fv(r)) * 16 + (q & 1) * 8);
+    }
+  }
+
+  // ---- running state of this lane's rows (both halves hold the same m)
+  f32x16 o[RB][NDB];
 #pragma unroll
-      for (int kp = 0; kp < NPK; ++kp) {
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16) * VSTR + db * 32));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vl + (kp * 16 + 8) * VSTR + db * 32));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kp], o[db], 0, 0, 0);
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[rb][db] = f32x16{};
+  float m_run[RB], l_run[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) { m_run[rb] = -INFINITY; l_run[rb] = 0.f; }
+  const float c = a.scale_log2;
+
+  // Q K^T for one 32-key half of the tile: every K fragment feeds each row block
+  auto qk_half = [&](const uint16_t* Ks, int h, f32x16 (&s)[RB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) s[rb] = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const bf16x8 kf = *(const bf16x8*)((const char*)Ks + h * 32 * RBY + k_rd[ks]);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[rb][ks], s[rb], 0, 0, 0);
+    }
+  };
+  // causal mask of one half (diagonal tiles only)
+  auto mask_half = [&](int k0h, f32x16 (&s)[RB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int kk = k0h + 8 * (v >> 2) + hh * 4 + (v & 3);
+        if (kk > key_lim[rb]) s[rb][v] = -INFINITY;
+      }
+  };
+  // row maxima of one half (scaled to log2 units); true if some row grew by more than 2^8
+  auto max_half = [&](f32x16 (&s)[RB], float (&mx)[RB]) __attribute__((always_inline)) {
+    bool grow = false;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) m = fmaxf(m, s[rb][v]);
+      mx[rb] = pair_max(m) * c;
+      grow |= mx[rb] > m_run[rb] + kRescaleThreshold;
+    }
+    return grow;
+  };
+  // rare: raise the running max and rescale O and l (wave-uniform branch)
+  auto rescale = [&](bool grow, const float (&mx)[RB]) __attribute__((always_inline)) {
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const float m_new = fmaxf(m_run[rb], mx[rb]);
+        const float alpha = (m_new == m_run[rb]) ? 1.f : __builtin_amdgcn_exp2f(m_run[rb] - m_new);
+        l_run[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[rb][db] *= alpha;
+        m_run[rb] = m_new;
       }
     }
   };
+  // exp2, row sums, bf16 pack of one half: pf[rb][kp] for the half's two 16-key steps
+  auto exp_half = [&](f32x16 (&s)[RB], bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float m_use = (m_run[rb] == -INFINITY) ? 0.f : m_run[rb];
+      float lsum = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][v], c, -m_use));
+        s[rb][v] = p;
+        lsum += p;
+      }
+      l_run[rb] += lsum;
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[rb][kp][e] = (__bf16)s[rb][kp * 8 + e];
+    }
+  };
+  // O^T += V^T P^T for one half: every V^T fragment feeds each row block
+  auto pv_half = [&](const uint16_t* Vs, int h, const bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp) {
+        const char* vp = (const char*)Vs + v_rd[db] + (h * 32 + kp * 16) * RBY;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * RBY));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[rb][kp], o[rb][db], 0, 0, 0);
+      }
+  };
 
-  // ---- key loop: one barrier per tile, next tile's loads in flight
-  if (t_lo < t_hi) {
-    load_tile(t_lo);
-    store_tile(0);
+  // One 64-key tile in two 32-key halves, ordered so that the matrix cores
+  // multiply one half while the VALU exponentiates the other:
+  //   QK(0) | max(0) | [QK(1) with exp(0)] [PV(0) with max(1)] | exp(1) | PV(1)
+  auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    f32x16 s0[RB], s1[RB];
+    float mx0[RB], mx1[RB];
+    bf16x8 p0[RB][2], p1[RB][2];
+    qk_half(Ks, 0, s0);
+    if constexpr (MASK) mask_half(k0, s0);
+    rescale(max_half(s0, mx0), mx0);
+    qk_half(Ks, 1, s1);
+    exp_half(s0, p0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA of QK(1)
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // six VALU ops of exp(0)
+    }
+    pv_half(Vs, 0, p0);
+    if constexpr (MASK) mask_half(k0 + 32, s1);
+    const bool grow1 = max_half(s1, mx1);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA of PV(0)
+      __builtin_amdgcn_sched_group_barrier(0x002, MASK ? 6 : 2, 0);   // VALU ops of max(1)
+    }
+    rescale(grow1, mx1);
+    exp_half(s1, p1);
+    pv_half(Vs, 1, p1);
+  };
+
+  // ---- key loop over the two buffers: tile t + 1 is loaded while tile t is
+  // multiplied; one barrier per tile.
+  auto step = [&](auto b, int t) __attribute__((always_inline)) {
+    constexpr int B = decltype(b)::value;
+    if (t + 1 < t_hi) load_tile(std::integral_constant<int, 1 - B>{}, t + 1);
+    const int k0 = t * BN;
+    if (wave_active && k0 <= wave_last_lim) {
+      if (k0 + BN - 1 > wave_first_lim)
+        compute_tile(kbuf(b), vbuf(b), k0, std::true_type{});
+      else
+        compute_tile(kbuf(b), vbuf(b), k0, std::false_type{});
+    }
+    __builtin_amdgcn_s_waitcnt(0);     // tile t + 1 has landed in the other buffer
     __syncthreads();
-    for (int t = t_lo; t < t_hi; ++t) {
-      const int buf = (t - t_lo) & 1;
-      const bool more = t + 1 < t_hi;
-      if (more) load_tile(t + 1);
-      const int k0 = t * BN;
-      if (wave_active && k0 <= wave_last_lim) compute_tile(buf, k0);
-      if (more) store_tile(buf ^ 1);
-      __syncthreads();
+  };
+  if (t_lo < t_hi) {
+    load_tile(std::integral_constant<int, 0>{}, t_lo);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int t = t_lo; t < t_hi; t += 2) {
+      step(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < t_hi) step(std::integral_constant<int, 1>{}, t + 1);
     }
   }
 
   if (!wave_active) return;
-  const float l_tot = pair_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse2 = l_tot > 0.f ? m_run + __log2f(l_tot) : -INFINITY;
-  if (row >= C) return;
-
-  if (a.splits == 1) {
-    if (a.out_f32) {
-      float* op = (float*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = wrow0 + rb * 32 + l32;
+    const float l_tot = pair_sum(l_run[rb]);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lse2 = l_tot > 0.f ? m_run[rb] + __log2f(l_tot) : -INFINITY;
+    if (row >= C) continue;
+    if (a.splits == 1) {
+      if (a.out_f32) {
+        float* op = (float*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          f32x4 v{o[db][q4 * 4] * inv, o[db][q4 * 4 + 1] * inv, o[db][q4 * 4 + 2] * inv, o[db][q4 * 4 + 3] * inv};
-          *(f32x4*)(op + db * 32 + q4 * 8) = v;
-        }
-    } else {
-      __bf16* op = (__bf16*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
+        for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const f32x16& x = o[rb][db];
+            *(f32x4*)(op + db * 32 + q4 * 8) =
+                f32x4{x[q4 * 4] * inv, x[q4 * 4 + 1] * inv, x[q4 * 4 + 2] * inv, x[q4 * 4 + 3] * inv};
+          }
+      } else {
+        __bf16* op = (__bf16*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-          bf16x4 v{(__bf16)(o[db][q4 * 4] * inv), (__bf16)(o[db][q4 * 4 + 1] * inv),
-                   (__bf16)(o[db][q4 * 4 + 2] * inv), (__bf16)(o[db][q4 * 4 + 3] * inv)};
-          *(bf16x4*)(op + db * 32 + q4 * 8) = v;
-        }
-    }
-    if (a.lse && hh == 0) a.lse[(int64_t)h * C + row] = lse2 * kLn2;
-  } else {
-    float* op = a.ws_o + (((int64_t)sp * a.Hq + h) * C + row) * D + hh * 4;
+        for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        f32x4 v{o[db][q4 * 4] * inv, o[db][q4 * 4 + 1] * inv, o[db][q4 * 4 + 2] * inv, o[db][q4 * 4 + 3] * inv};
-        *(f32x4*)(op + db * 32 + q4 * 8) = v;
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const f32x16& x = o[rb][db];
+            *(bf16x4*)(op + db * 32 + q4 * 8) =
+                bf16x4{(__bf16)(x[q4 * 4] * inv), (__bf16)(x[q4 * 4 + 1] * inv), (__bf16)(x[q4 * 4 + 2] * inv),
+                       (__bf16)(x[q4 * 4 + 3] * inv)};
+          }
       }
-    if (hh == 0) a.ws_lse[((int64_t)sp * a.Hq + h) * C + row] = lse2;
+      if (a.lse && hh == 0) a.lse[(int64_t)h * C + row] = lse2 * kLn2;
+    } else {
+      float* op = a.ws_o + (((int64_t)sp * a.Hq + h) * C + row) * D + hh * 4;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const f32x16& x = o[rb][db];
+          *(f32x4*)(op + db * 32 + q4 * 8) =
+              f32x4{x[q4 * 4] * inv, x[q4 * 4 + 1] * inv, x[q4 * 4 + 2] * inv, x[q4 * 4 + 3] * inv};
+        }
+      if (hh == 0) a.ws_lse[((int64_t)sp * a.Hq + h) * C + row] = lse2;
+    }
   }
 }
 
@@ -380,7 +519,6 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   if (a.out_f32) {
     *(f32x4*)((float*)a.out + oo) = acc;
   } else {
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     *(bf16x4*)((__bf16*)a.out + oo) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
   }
   if (dq == 0 && a.lse) a.lse[(int64_t)h * a.C + row] = wsum > 0.f ? (m_use + __log2f(wsum)) * kLn2 : -INFINITY;

@@ -7,17 +7,19 @@
 namespace vico {
 
 // Tile geometry of the attention kernel.  A work-group of 4 waves owns
-// kBlockM = 128 query rows of one query head; each wave owns 32 rows.
-// Keys are walked in tiles of 8192 / head_dim keys so that a K tile plus a
-// V tile always take 32 KiB of LDS (double-buffered: 2 work-groups per CU
-// fit in the 160 KiB of LDS).
-constexpr int kBlockM = 128;
+// kBlockM = 128 query rows of one query head; each wave owns kRowBlocks = 1
+// block of 32 rows.  Keys are walked in tiles of kKeyTile = 64, double-
+// buffered in LDS (64 KiB per work-group at head_dim 128); two work-groups
+// share a CU, so each SIMD interleaves two waves.
 constexpr int kThreads = 256;
+constexpr int kRowBlocks = 1;
+constexpr int kBlockM = 4 * kRowBlocks * 32;
+constexpr int kKeyTile = 64;
 constexpr int kNumCUs = 256;        // MI355X: 8 XCDs x 32 CUs
 constexpr int kWgPerCU = 2;
 constexpr int kMaxSplits = 16;
 
-inline int key_tile(int head_dim) { return 8192 / head_dim; }
+inline int key_tile(int) { return kKeyTile; }
 
 // Everything the attention kernels need, resolved on the host.
 struct AttnArgs {

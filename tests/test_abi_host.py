@@ -122,8 +122,8 @@ def test_plan_for_the_workloads(cfg, splits):
 
 
 def test_forced_splits_are_clamped_to_the_key_tiles():
-    # 16 + 256 + 64 keys in tiles of 128 keys (head_dim 64) -> at most 3 splits
-    assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=8)[0] == 3
+    # 16 + 256 + 64 keys in tiles of 64 keys -> at most 6 splits
+    assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=8)[0] == 6
     assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=2)[0] == 2
     with pytest.raises(vico.VicoError):
         vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=-3)
