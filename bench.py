@@ -292,7 +292,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--traffic-bytes", type=float, default=None,
                     help="HBM bytes per attention launch from rocprofv3 FETCH_SIZE+WRITE_SIZE, if measured")
     args = ap.parse_args()

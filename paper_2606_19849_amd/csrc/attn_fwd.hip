@@ -390,32 +390,31 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   // One 64-key tile in two 32-key halves, ordered so that the matrix cores
   // multiply one half while the VALU exponentiates the other:
   //   QK(0) | max(0) | [QK(1) with exp(0)] [PV(0) with max(1)] | exp(1) | PV(1)
+  // The wave raises its issue priority while it feeds the matrix cores, so of
+  // the two waves sharing a SIMD the one with MFMAs ready goes first and the
+  // other's softmax VALU work fills the MFMA shadow.
   auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
     f32x16 s0[RB], s1[RB];
     float mx0[RB], mx1[RB];
     bf16x8 p0[RB][2], p1[RB][2];
+    __builtin_amdgcn_s_setprio(1);
     qk_half(Ks, 0, s0);
+    __builtin_amdgcn_s_setprio(0);
     if constexpr (MASK) mask_half(k0, s0);
     rescale(max_half(s0, mx0), mx0);
+    __builtin_amdgcn_s_setprio(1);
     qk_half(Ks, 1, s1);
     exp_half(s0, p0);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA of QK(1)
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // six VALU ops of exp(0)
-    }
     pv_half(Vs, 0, p0);
     if constexpr (MASK) mask_half(k0 + 32, s1);
     const bool grow1 = max_half(s1, mx1);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA of PV(0)
-      __builtin_amdgcn_sched_group_barrier(0x002, MASK ? 6 : 2, 0);   // VALU ops of max(1)
-    }
+    __builtin_amdgcn_s_setprio(0);
     rescale(grow1, mx1);
     exp_half(s1, p1);
+    __builtin_amdgcn_s_setprio(1);
     pv_half(Vs, 1, p1);
+    __builtin_amdgcn_s_setprio(0);
   };
 
   // ---- key loop over the two buffers: tile t + 1 is loaded while tile t is
