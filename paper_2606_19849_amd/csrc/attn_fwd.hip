@@ -7,10 +7,10 @@
 // at token granularity, causal inside the chunk).
 //
 // Mapping onto the hardware
-//   * Work-group = 4 waves, one per SIMD (each wave may use the whole 512-entry
-//     register file), = 256 query rows of one query head (one key range when
-//     split).  Each wave owns 64 rows -- two 32-row MFMA blocks -- for the
-//     whole key loop, so every K and V fragment read from LDS feeds two MFMAs.
+//   * Work-group = 8 waves (two per SIMD, one work-group per CU) = 256 query
+//     rows of one query head (one key range when split).  Each wave owns 32
+//     rows for the whole key loop; every K/V tile brought into LDS serves all
+//     256 rows.
 //   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: the K tile (from LDS) is the
 //     A operand, the wave's Q rows (held in VGPRs for the whole loop) the B
 //     operand.  In the accumulator layout lane l then holds 16 logits of
@@ -101,7 +101,7 @@ constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n_rt, int g) {
+__global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a, int n_rt, int g) {
   constexpr int BN = kKeyTile;         // keys per tile
   constexpr int RB = kRowBlocks;       // 32-row blocks per wave
   constexpr int BM = kBlockM;          // rows per work-group
@@ -118,24 +118,31 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   constexpr int RBY = D * 2;           // bytes per LDS row
   constexpr int KT = BN * D;           // elements of one K (or V) tile
   constexpr int VT = BN * D;
-  constexpr int NLD = BN * RBY / 1024 / 4;   // direct 1 KiB loads per wave per tile (K or V)
+  constexpr int NW = kThreads / 64;          // waves per work-group
+  constexpr int NLD = BN * RBY / 1024 / NW;  // direct 1 KiB loads per wave per tile (K or V)
   constexpr int RPL = 1024 / RBY;            // rows per direct load
-  static_assert(NLD * 4 * 1024 == BN * RBY, "direct loads cover the tile");
+  constexpr int NBUF = kBuffers;
+  static_assert(NLD * NW * 1024 == BN * RBY, "direct loads cover the tile");
+  static_assert(BM == NW * RB * 32, "work-group rows");
+  static_assert(NBUF == 2 || NBUF == 3, "two or three LDS buffers");
+  static_assert(BN % 64 == 0, "key tiles are whole 64-key sub-tiles");
   auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
   auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
 
-  // Two K/V buffers (tile t in buffer t mod 2; the next tile loads while this
-  // one is multiplied).  Separate arrays let the compiler see that reads of
-  // one buffer do not wait for the direct loads landing in the other.
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds0[KT], k_lds1[KT];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds0[VT], v_lds1[VT];
+  // NBUF K/V buffers: tile t lives in buffer t mod NBUF and is loaded NBUF-1
+  // tiles ahead.  Separate arrays let the compiler see that reads of one
+  // buffer do not wait for the direct loads landing in another.
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds0[KT], k_lds1[KT], k_lds2[NBUF > 2 ? KT : 1];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds0[VT], v_lds1[VT], v_lds2[NBUF > 2 ? VT : 1];
   auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
     if constexpr (decltype(b)::value == 0) return k_lds0;
-    else return k_lds1;
+    else if constexpr (decltype(b)::value == 1) return k_lds1;
+    else return k_lds2;
   };
   auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
     if constexpr (decltype(b)::value == 0) return v_lds0;
-    else return v_lds1;
+    else if constexpr (decltype(b)::value == 1) return v_lds1;
+    else return v_lds2;
   };
 
   const int tid = threadIdx.x;
@@ -194,7 +201,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
   uint32_t ld_ck[NLD], ld_cv[NLD];  // byte offset of the fetched K / V unit inside a token row
 #pragma unroll
   for (int n = 0; n < NLD; ++n) {
-    const int r = wave * (BN / 4) + n * RPL + lane / UPR;
+    const int r = wave * (BN / NW) + n * RPL + lane / UPR;
     const int pu = lane % UPR;
     ld_row[n] = r;
     ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ fk(r)) * 16);
@@ -227,8 +234,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
 #pragma unroll
     for (int n = 0; n < NLD; ++n) {
       const uint32_t rowoff = (uint32_t)(row_base + ld_row[n]) * (uint32_t)rbytes;
-      lds_void* kd = (lds_void*)(Ks + (wave * (BN / 4) + n * RPL) * D);
-      lds_void* vd = (lds_void*)(Vs + (wave * (BN / 4) + n * RPL) * D);
+      lds_void* kd = (lds_void*)(Ks + (wave * (BN / NW) + n * RPL) * D);
+      lds_void* vd = (lds_void*)(Vs + (wave * (BN / NW) + n * RPL) * D);
       load_lds16(rk_, kd, rowoff + ld_ck[n]);
       load_lds16(rv_, vd, rowoff + ld_cv[n]);
     }
@@ -417,28 +424,45 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a, int n
     __builtin_amdgcn_s_setprio(0);
   };
 
-  // ---- key loop over the two buffers: tile t + 1 is loaded while tile t is
+  // ---- key loop over the buffers: tile t + NBUF - 1 is loaded while tile t is
   // multiplied; one barrier per tile.
+  constexpr uint32_t kWaitNewestTile = 0x0F70u | (uint32_t)(2 * NLD);   // vmcnt(2*NLD)
   auto step = [&](auto b, int t) __attribute__((always_inline)) {
     constexpr int B = decltype(b)::value;
-    if (t + 1 < t_hi) load_tile(std::integral_constant<int, 1 - B>{}, t + 1);
-    const int k0 = t * BN;
-    if (wave_active && k0 <= wave_last_lim) {
-      if (k0 + BN - 1 > wave_first_lim)
-        compute_tile(kbuf(b), vbuf(b), k0, std::true_type{});
-      else
-        compute_tile(kbuf(b), vbuf(b), k0, std::false_type{});
+    bool async_next = false;
+    if (t + NBUF - 1 < t_hi) async_next = load_tile(std::integral_constant<int, (B + NBUF - 1) % NBUF>{}, t + NBUF - 1);
+    // the tile body works on 64-key sub-tiles (the operand swizzles only
+    // depend on the row modulo 16, so a sub-tile is addressed from its base)
+#pragma unroll
+    for (int sub = 0; sub < BN / 64; ++sub) {
+      const int k0 = t * BN + sub * 64;
+      const uint16_t* Ks = kbuf(b) + sub * 64 * D;
+      const uint16_t* Vs = vbuf(b) + sub * 64 * D;
+      if (wave_active && k0 <= wave_last_lim) {
+        if (k0 + 63 > wave_first_lim)
+          compute_tile(Ks, Vs, k0, std::true_type{});
+        else
+          compute_tile(Ks, Vs, k0, std::false_type{});
+      }
     }
-    __builtin_amdgcn_s_waitcnt(0);     // tile t + 1 has landed in the other buffer
+    // Tile t + 1 must have landed.  With three buffers the newest tile's
+    // direct loads (issued above, if any) may stay in flight.
+    if (NBUF == 3 && async_next)
+      __builtin_amdgcn_s_waitcnt(kWaitNewestTile);
+    else
+      __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   };
   if (t_lo < t_hi) {
     load_tile(std::integral_constant<int, 0>{}, t_lo);
+    if (NBUF == 3 && t_lo + 1 < t_hi) load_tile(std::integral_constant<int, 1>{}, t_lo + 1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int t = t_lo; t < t_hi; t += 2) {
+    for (int t = t_lo; t < t_hi; t += NBUF) {
       step(std::integral_constant<int, 0>{}, t);
       if (t + 1 < t_hi) step(std::integral_constant<int, 1>{}, t + 1);
+      if constexpr (NBUF == 3)
+        if (t + 2 < t_hi) step(std::integral_constant<int, 2 % NBUF>{}, t + 2);
     }
   }
 

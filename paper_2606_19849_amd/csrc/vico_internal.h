@@ -6,17 +6,18 @@
 
 namespace vico {
 
-// Tile geometry of the attention kernel.  A work-group of 4 waves owns
-// kBlockM = 128 query rows of one query head; each wave owns kRowBlocks = 1
-// block of 32 rows.  Keys are walked in tiles of kKeyTile = 64, double-
-// buffered in LDS (64 KiB per work-group at head_dim 128); two work-groups
-// share a CU, so each SIMD interleaves two waves.
-constexpr int kThreads = 256;
+// Tile geometry of the attention kernel.  A work-group of 8 waves (two per
+// SIMD) owns kBlockM = 256 query rows of one query head; each wave owns
+// kRowBlocks = 1 block of 32 rows.  Keys are walked in tiles of kKeyTile,
+// double-buffered in LDS (32 KiB per 64 keys at head_dim 128); one
+// work-group per CU, so every K/V tile in LDS serves 256 rows.
+constexpr int kThreads = 512;
 constexpr int kRowBlocks = 1;
-constexpr int kBlockM = 4 * kRowBlocks * 32;
+constexpr int kBlockM = (kThreads / 64) * kRowBlocks * 32;
 constexpr int kKeyTile = 64;
+constexpr int kBuffers = 2;
 constexpr int kNumCUs = 256;        // MI355X: 8 XCDs x 32 CUs
-constexpr int kWgPerCU = 2;
+constexpr int kWgPerCU = 1;
 constexpr int kMaxSplits = 16;
 
 inline int key_tile(int) { return kKeyTile; }
