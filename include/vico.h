@@ -54,6 +54,7 @@ typedef enum {
 enum { VICO_DTYPE_BF16 = 0, VICO_DTYPE_F32 = 1 };
 
 #define VICO_FULL_HISTORY (-1)
+#define VICO_SPLIT_BALANCED (-1)
 
 /*
  * vico_kv_append -- append a chunk's K/V to the ring-buffer visual cache.
@@ -99,10 +100,12 @@ int vico_kv_append(const void* k_chunk, const void* v_chunk, int32_t chunk_len,
  *                  nearest even) or F32
  *   lse_out        NULL or [num_q_heads][chunk_len] fp32: natural-log sum of
  *                  exp(scale * q.k) over the visible keys of each row
- *   num_splits     0: the library picks how many key ranges to split each row
- *                  tile into (more work-groups for small chunks); n > 0 forces n
- *                  (clamped to the number of key tiles).  Results agree up to
- *                  rounding for every n.
+ *   num_splits     0: the library picks the schedule; n > 0 splits every row
+ *                  tile's key range into n parts (clamped to the number of key
+ *                  tiles); VICO_SPLIT_BALANCED gives every work-group an equal
+ *                  share of all key tiles of all row tiles.  Split or shared
+ *                  row tiles are combined by a log-sum-exp merge.  Results
+ *                  agree up to rounding for every choice.
  *   workspace      device scratch of at least vico_attn_workspace_bytes(...) bytes
  *                  for the same arguments; may be NULL when that size is 0.
  *
@@ -122,7 +125,7 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
 /*
  * vico_attn_plan -- how vico_chunk_prefill_attn will run for these arguments.
  * Host-only; validates the shape arguments exactly as the attention call does.
- *   *num_splits_out      key-range splits per row tile (1 = no split)
+ *   *num_splits_out      partial results merged per row (1 = no merge)
  *   *workspace_bytes_out device scratch the call needs (0 when not split)
  * Either output pointer may be NULL.
  */

@@ -11,6 +11,7 @@ from ._binding import (
     VICO_DTYPE_BF16,
     VICO_DTYPE_F32,
     VICO_FULL_HISTORY,
+    VICO_SPLIT_BALANCED,
     VicoError,
     load_library,
     header_functions,
@@ -24,6 +25,7 @@ __all__ = [
     "VICO_DTYPE_BF16",
     "VICO_DTYPE_F32",
     "VICO_FULL_HISTORY",
+    "VICO_SPLIT_BALANCED",
     "VicoError",
     "load_library",
     "header_functions",

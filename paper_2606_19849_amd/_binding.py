@@ -20,6 +20,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "vico.h")
 VICO_DTYPE_BF16 = 0
 VICO_DTYPE_F32 = 1
 VICO_FULL_HISTORY = -1
+VICO_SPLIT_BALANCED = -1
 
 _i32, _i64, _f32, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
 

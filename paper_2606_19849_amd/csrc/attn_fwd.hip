@@ -151,22 +151,21 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   const int l32 = lane & 31;
   const int hh = lane >> 5;
 
-  // ---- which rows / head / key range this work-group owns
-  const int L = xcd_remap(blockIdx.x, gridDim.x);
-  const int qh = L % g;
-  int rest = L / g;
-  const int rt = n_rt - 1 - rest % n_rt;   // longest row tiles first
-  rest /= n_rt;
-  const int sp = rest % a.splits;
-  const int kv = rest / a.splits;
-  const int h = kv * g + qh;
-
   const int C = a.C, S = a.S, SW = a.S + a.Wv;
+  // key tiles seen by row tile rt: keys up to the last row's own position
+  auto tiles_of = [&](int rt) __attribute__((always_inline)) {
+    return (SW + min((rt + 1) * BM, C) + BN - 1) / BN;
+  };
+
+  // ---- one segment of work: key tiles [t_lo, t_hi) of row tile rt of query
+  // head h = kv*g + qh.  `partial` segments write fp32 O and log2-sum-exp to
+  // workspace slot `part` (of n_parts) for the merge kernel; others write the
+  // output.  All waves of the work-group run the same segments.
+  auto segment = [&](int kv, int rt, int qh, int t_lo, int t_hi, int part, int n_parts, bool partial)
+      __attribute__((always_inline)) {
+  const int h = kv * g + qh;
   const int row0 = rt * BM;
-  const int row_last = min(row0 + BM, C) - 1;
-  const int n_tiles = (SW + row_last + 1 + BN - 1) / BN;
-  const int t_lo = (int)((int64_t)n_tiles * sp / a.splits);
-  const int t_hi = (int)((int64_t)n_tiles * (sp + 1) / a.splits);
+  const int n_tiles = tiles_of(rt);
 
   // this wave: rows wrow0 + rb*32 + l32, rb < RB
   const int wrow0 = row0 + wave * 32 * RB;
@@ -474,7 +473,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     const float lse2 = l_tot > 0.f ? m_run[rb] + __log2f(l_tot) : -INFINITY;
     if (row >= C) continue;
-    if (a.splits == 1) {
+    if (!partial) {
       if (a.out_f32) {
         float* op = (float*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
 #pragma unroll
@@ -499,7 +498,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
       }
       if (a.lse && hh == 0) a.lse[(int64_t)h * C + row] = lse2 * kLn2;
     } else {
-      float* op = a.ws_o + (((int64_t)sp * a.Hq + h) * C + row) * D + hh * 4;
+      float* op = a.ws_o + (((int64_t)part * a.Hq + h) * C + row) * D + hh * 4;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -508,7 +507,65 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
           *(f32x4*)(op + db * 32 + q4 * 8) =
               f32x4{x[q4 * 4] * inv, x[q4 * 4 + 1] * inv, x[q4 * 4 + 2] * inv, x[q4 * 4 + 3] * inv};
         }
-      if (hh == 0) a.ws_lse[((int64_t)sp * a.Hq + h) * C + row] = lse2;
+      if (hh == 0) {
+        a.ws_lse[((int64_t)part * a.Hq + h) * C + row] = lse2;
+        // a row tile that ends in this segment uses no later parts
+        if (t_hi == n_tiles)
+          for (int p2 = part + 1; p2 < n_parts; ++p2) a.ws_lse[((int64_t)p2 * a.Hq + h) * C + row] = -INFINITY;
+      }
+    }
+  }
+  };   // segment
+
+  // ---- schedule
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  if (!a.balanced) {
+    // one row tile (one key range of it when split) per work-group
+    const int qh = L % g;
+    int rest = L / g;
+    const int rt = n_rt - 1 - rest % n_rt;   // longest row tiles first
+    rest /= n_rt;
+    const int sp = rest % a.splits;
+    const int kv = rest / a.splits;
+    const int nt = tiles_of(rt);
+    const int t_lo = (int)((int64_t)nt * sp / a.splits);
+    const int t_hi = (int)((int64_t)nt * (sp + 1) / a.splits);
+    segment(kv, rt, qh, t_lo, t_hi, sp, a.splits, a.splits > 1);
+  } else {
+    // Balanced: the (row tile, key tile) pairs of all row tiles, in the order
+    // kv, row tile (longest first), query head, are cut into gridDim.x equal
+    // ranges.  A row tile cut between work-groups is finished by the merge
+    // kernel; part = index of the work-group among those covering it.
+    const int64_t G = gridDim.x, T = a.total_tiles;
+    int64_t pos = (int64_t)L * T / G;
+    const int64_t end = (int64_t)(L + 1) * T / G;
+    bool first = true;
+    while (pos < end) {
+      int64_t base = 0;
+      int kv = 0, rt = 0, qh = 0, nt = 1;
+      for (int k = 0; k < a.Hkv; ++k)
+        for (int ri = 0; ri < n_rt; ++ri) {
+          const int r = n_rt - 1 - ri;
+          const int n = tiles_of(r);
+          const int64_t blk = (int64_t)g * n;
+          if (pos >= base && pos < base + blk) {
+            kv = k; rt = r; nt = n; qh = (int)((pos - base) / n);
+          }
+          base += blk;
+        }
+      // start of the containing row tile in the global order
+      int64_t task_start = 0;
+      for (int k = 0; k < kv; ++k)
+        for (int ri = 0; ri < n_rt; ++ri) task_start += (int64_t)g * tiles_of(ri);
+      for (int ri = 0; ri < n_rt - 1 - rt; ++ri) task_start += (int64_t)g * tiles_of(n_rt - 1 - ri);
+      task_start += (int64_t)qh * nt;
+      const int lo = (int)(pos - task_start);
+      const int hi = (int)(min(end, task_start + nt) - task_start);
+      const int owner = (int)(((task_start + 1) * G - 1) / T);   // work-group holding the row tile's first key tile
+      if (!first) __syncthreads();      // the previous segment is done with the LDS buffers
+      segment(kv, rt, qh, lo, hi, L - owner, a.splits, true);
+      first = false;
+      pos = task_start + hi;
     }
   }
 }
@@ -531,7 +588,9 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   f32x4 acc{0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
   for (int s = 0; s < a.splits; ++s) {
-    const float w = __builtin_amdgcn_exp2f(a.ws_lse[s * stride_s + hr] - m_use);
+    const float ls = a.ws_lse[s * stride_s + hr];
+    if (ls == -INFINITY) continue;      // empty part: its O slot may never have been written
+    const float w = __builtin_amdgcn_exp2f(ls - m_use);
     const f32x4 v = *(const f32x4*)(a.ws_o + (s * stride_s + hr) * D + dq * 4);
     wsum += w;
     acc += w * v;
@@ -549,14 +608,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
+hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream) {
   const int g = a.Hq / a.Hkv;
   const int n_rt = (a.C + kBlockM - 1) / kBlockM;
-  const int nwg = a.Hq * n_rt * a.splits;
   if (a.D == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(nwg), dim3(kThreads), 0, stream, a, n_rt, g);
+    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a, n_rt, g);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(nwg), dim3(kThreads), 0, stream, a, n_rt, g);
+    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a, n_rt, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || a.splits == 1) return err;
   const int64_t total = (int64_t)a.Hq * a.C * (a.D / 4);

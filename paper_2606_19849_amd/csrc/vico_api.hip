@@ -3,6 +3,8 @@
 // every buffer, the workspace included, belongs to the caller.
 
 #include <math.h>
+
+#include <algorithm>
 #include <stdint.h>
 
 #include "vico.h"
@@ -25,30 +27,64 @@ bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
 }
 
 struct Shape {
-  int C, S, R, Wv, ws, Hq, Hkv, D, splits;
+  int C, S, R, Wv, ws, Hq, Hkv, D, splits, balanced, grid;
+  int64_t total_tiles;
   int64_t ws_bytes;
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
-int plan_splits(int C, int S, int Wv, int Hq, int D, int request) {
-  const int BN = vico::key_tile(D);
+int64_t tiles_of(int rt, int C, int SW) {
+  const int64_t last = std::min<int64_t>(int64_t(rt + 1) * vico::kBlockM, C);
+  return (SW + last + vico::kKeyTile - 1) / vico::kKeyTile;
+}
+
+// Splits of every row tile's key range (power of two), chosen while the grid
+// stays within one round of resident work-groups and each split keeps at
+// least 16 key tiles.
+int plan_splits(int C, int S, int Wv, int Hq, int request) {
   const int64_t n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
   const int64_t wgs = int64_t(Hq) * n_rt;
-  const int64_t tiles = (int64_t(S) + Wv + C + BN - 1) / BN;
+  const int64_t tiles = (int64_t(S) + Wv + C + vico::kKeyTile - 1) / vico::kKeyTile;
   const int64_t cap = tiles < vico::kMaxSplits ? tiles : vico::kMaxSplits;
   if (request > 0) return (int)(request < cap ? request : cap);
-  // Split only while the grid stays within one round of resident work-groups
-  // and every split keeps at least 16 key tiles.
   int ns = 1;
   while (ns * 2 <= cap && wgs * ns * 2 <= int64_t(vico::kNumCUs) * vico::kWgPerCU && tiles >= 16 * ns * 2) ns *= 2;
   return ns;
 }
 
+// Balanced plan: gridDim.x equal shares of the (row tile, key tile) pairs.
+// Returns the largest number of work-groups any row tile is spread over, or
+// 0 when the balanced schedule does not apply.
+int plan_balanced(int C, int SW, int Hq, int Hkv, int64_t* total, int* grid) {
+  const int n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
+  const int g = Hq / Hkv;
+  int64_t T = 0;
+  for (int rt = 0; rt < n_rt; ++rt) T += int64_t(Hq) * tiles_of(rt, C, SW);
+  const int64_t G = int64_t(vico::kNumCUs) * vico::kWgPerCU;
+  if (T < 4 * G) return 0;
+  // walk the row tiles in kernel order: kv, row tile (longest first), query head
+  int max_parts = 1;
+  int64_t start = 0;
+  for (int kv = 0; kv < Hkv; ++kv)
+    for (int ri = 0; ri < n_rt; ++ri) {
+      const int64_t n = tiles_of(n_rt - 1 - ri, C, SW);
+      for (int qh = 0; qh < g; ++qh) {
+        const int64_t w0 = ((start + 1) * G - 1) / T, w1 = ((start + n) * G - 1) / T;
+        max_parts = (int)std::max<int64_t>(max_parts, w1 - w0 + 1);
+        start += n;
+      }
+    }
+  if (max_parts > vico::kMaxSplits) return 0;
+  *total = T;
+  *grid = (int)G;
+  return max_parts;
+}
+
 // Validates everything the attention call and the planner share.
 int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int32_t Hq, int32_t Hkv,
                      int32_t D, int32_t splits, Shape* sh) {
-  if (C < 0 || S < 0 || R < 0 || H < 0 || W < -1 || splits < 0) return VICO_ERR_INVALID_ARG;
+  if (C < 0 || S < 0 || R < 0 || H < 0 || W < -1 || splits < VICO_SPLIT_BALANCED) return VICO_ERR_INVALID_ARG;
   if (Hq < 1 || Hkv < 1 || Hq > kMaxHeads || Hq % Hkv != 0) return VICO_ERR_INVALID_ARG;
   if (D != 64 && D != 128) return VICO_ERR_UNSUPPORTED;
   if (C > kMaxChunk || S > kMaxChunk) return VICO_ERR_INVALID_ARG;
@@ -62,7 +98,28 @@ int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int3
   sh->C = C; sh->S = S; sh->R = R; sh->Wv = (int)wv;
   sh->ws = R > 0 ? (int)((H - wv) % R) : 0;
   sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;
-  sh->splits = C > 0 ? plan_splits(C, S, (int)wv, Hq, D, splits) : 1;
+  sh->splits = 1;
+  sh->balanced = 0;
+  sh->total_tiles = 0;
+  sh->grid = 0;
+  if (C > 0) {
+    const int64_t n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
+    const int ns = splits == VICO_SPLIT_BALANCED ? 1 : plan_splits(C, S, (int)wv, Hq, splits);
+    int parts = 0;
+    // balanced when asked for, or when the split grid would leave at least half
+    // the CUs idle (measured: with most CUs busy the merge costs what the
+    // balance gains -- the chip runs power-limited and idle CUs raise the clock)
+    if (splits == VICO_SPLIT_BALANCED ||
+        (splits == 0 && 2 * int64_t(Hq) * n_rt * ns <= int64_t(vico::kNumCUs) * vico::kWgPerCU))
+      parts = plan_balanced(C, S + (int)wv, Hq, Hkv, &sh->total_tiles, &sh->grid);
+    if (parts > 0) {
+      sh->balanced = 1;
+      sh->splits = parts;
+    } else {
+      sh->splits = ns;
+      sh->grid = (int)(int64_t(Hq) * n_rt * ns);
+    }
+  }
   sh->ws_bytes = sh->splits > 1
                      ? align256(int64_t(4) * sh->splits * Hq * C * D) + int64_t(4) * sh->splits * Hq * C
                      : 0;
@@ -167,10 +224,12 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
   a.C = sh.C; a.S = sh.S; a.R = sh.R; a.Wv = sh.Wv; a.ws = sh.ws;
   a.Hq = sh.Hq; a.Hkv = sh.Hkv; a.D = sh.D;
   a.splits = sh.splits;
+  a.balanced = sh.balanced;
+  a.total_tiles = sh.total_tiles;
   a.out_f32 = out_dtype == VICO_DTYPE_F32;
   const double scale = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(head_dim));
   a.scale_log2 = (float)(scale * 1.4426950408889634);
-  const hipError_t e = vico::launch_attention(a, (hipStream_t)stream);
+  const hipError_t e = vico::launch_attention(a, sh.grid, (hipStream_t)stream);
   return e == hipSuccess ? VICO_OK : hip_fail(e);
 }
 

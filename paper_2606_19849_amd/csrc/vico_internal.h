@@ -37,7 +37,9 @@ struct AttnArgs {
   float* ws_lse;       // [splits][Hq][C] fp32 (log2 units)
   int C, S, R, Wv, ws; // ws = first window slot = (H - Wv) mod R
   int Hq, Hkv, D;
-  int splits;
+  int splits;          // partial results per row merged at the end (1: none)
+  int balanced;        // 1: work-groups take equal shares of all key tiles
+  int64_t total_tiles; // balanced mode: key tiles summed over all row tiles and heads
   int out_f32;
   float scale_log2;    // softmax scale * log2(e)
 };
@@ -51,7 +53,7 @@ struct AppendArgs {
   int row_elems;       // Hkv * D
 };
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 
 }  // namespace vico
