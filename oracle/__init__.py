@@ -17,9 +17,11 @@ Modules
   attention  -- exact masked softmax attention (blocked and per-row forms)
   ring       -- linear-history model of the ring-buffer KV cache
   merge      -- log-sum-exp merge of attention over disjoint key sets
+  retrieval  -- query-side chunk retrieval (token means, cosine scores,
+                top-k selection) and attention over the retrieved chunks
 
 Parity status: every function here is pinned by tests in
-tests/test_oracle_pins.py against library routines, closed forms,
+tests/test_oracle_pins.py and tests/test_oracle_retrieval_pins.py against library routines, closed forms,
 invariants and brute force; none is "parity unpinned".
 """
 from .bf16 import bf16_bits_to_f64
@@ -32,6 +34,7 @@ from .attention import (
 )
 from .ring import RingModel
 from .merge import lse_merge
+from .retrieval import token_mean, cosine_scores, select_chunks, chunk_segments, gather_attention
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -42,4 +45,9 @@ __all__ = [
     "kv_head_of",
     "RingModel",
     "lse_merge",
+    "token_mean",
+    "cosine_scores",
+    "select_chunks",
+    "chunk_segments",
+    "gather_attention",
 ]

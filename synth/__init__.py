@@ -27,6 +27,11 @@ __all__ = [
     "ragged_chunk_lengths",
     "stream_chunk",
     "CONFIGS",
+    "QueryShape",
+    "QueryInputs",
+    "make_query_inputs",
+    "make_tokens",
+    "QUERY_CONFIGS",
 ]
 
 
@@ -162,4 +167,117 @@ CONFIGS = {
     # full history (65536 tokens) vs bounded W = 8192 at 3B heads, chunk 2048.
     "full": ChunkShape(16, 2, 128, 64, 65536, 65536, -1, 2048),
     "full_bounded": ChunkShape(16, 2, 128, 64, 65536, 65536, 8192, 2048),
+}
+
+
+# ---------------------------------------------------------------------------
+# Query-side retrieval workloads: a store of past chunks (linear history of
+# K/V), one representative feature per chunk, and a short query.
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class QueryShape:
+    """Shape of one query-side call (retrieval + attention over retrieved chunks).
+
+    feat_dim is the LLM hidden size of the representative features; the store
+    holds num_chunks chunks of ragged length in [chunk_lo, chunk_hi], stored one
+    after another; q_len query rows are the last of tail_len tail tokens."""
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    sink_len: int
+    feat_dim: int
+    num_chunks: int
+    chunk_lo: int
+    chunk_hi: int
+    q_len: int
+    tail_len: int
+    top_k: int
+
+
+@dataclass
+class QueryInputs:
+    shape: QueryShape
+    chunk_len: np.ndarray      # [N] int64 retained tokens per chunk
+    chunk_start: np.ndarray    # [N] int64 first store slot of each chunk
+    chunk_feat: np.ndarray     # [N, dm] float32 representative features
+    query_x: np.ndarray        # [Lq, dm] bf16 bits: query token embeddings
+    q: np.ndarray              # [Lq, Hq, d] bf16 bits
+    tail_k: np.ndarray         # [T, Hkv, d]
+    tail_v: np.ndarray
+    sink_k: np.ndarray         # [S, Hkv, d]
+    sink_v: np.ndarray
+    seed: int = 0
+    family: str = "F1"
+
+    @property
+    def store_len(self) -> int:
+        return int(self.chunk_start[-1] + self.chunk_len[-1]) if len(self.chunk_len) else 0
+
+    def chunk_kv(self, i: int):
+        """K/V bits of stored chunk i, drawn from PCG64([seed, 3, i]) in order K, V."""
+        sh = self.shape
+        _, sk, sv = _family_sigmas(self.family, sh.head_dim)
+        rng = np.random.Generator(np.random.PCG64([self.seed, 3, i]))
+        n = int(self.chunk_len[i])
+        return (_draw(rng, (n, sh.num_kv_heads, sh.head_dim), sk),
+                _draw(rng, (n, sh.num_kv_heads, sh.head_dim), sv))
+
+    def store_kv(self):
+        """The whole store [store_len, Hkv, d] (K, V), chunk after chunk."""
+        ks, vs = zip(*(self.chunk_kv(i) for i in range(len(self.chunk_len))))
+        return np.concatenate(ks, axis=0), np.concatenate(vs, axis=0)
+
+
+def _family_sigmas(family: str, d: int):
+    if family == "F1":
+        return (1.0 / np.sqrt(d),) * 3
+    if family == "F2":
+        return 2.0, 2.0, 1.0
+    raise ValueError(f"unknown input family {family!r}")
+
+
+def make_query_inputs(shape: QueryShape, seed=0, family: str = "F1", num_topics: int = 16) -> QueryInputs:
+    """Draw a query-side workload.
+
+    Features follow a topic mixture so that similarities spread out: topic
+    vectors t_j ~ N(0,1); chunk i gets a topic and feature t + 0.75 N(0,1);
+    the query tokens are t_q + N(0,1) for one topic t_q.  Streams:
+    PCG64([seed, 1]) lengths and features, PCG64([seed, 2]) query tokens,
+    q and tail, PCG64([seed, 3, i]) chunk i's K/V, PCG64([seed, 4]) sink."""
+    sh = shape
+    sq, sk, sv = _family_sigmas(family, sh.head_dim)
+    rng = np.random.Generator(np.random.PCG64([seed, 1]))
+    lens = rng.integers(sh.chunk_lo, sh.chunk_hi + 1, sh.num_chunks).astype(np.int64)
+    start = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    topics = rng.standard_normal((num_topics, sh.feat_dim), dtype=np.float32)
+    which = rng.integers(0, num_topics, sh.num_chunks)
+    feat = (topics[which] + np.float32(0.75) * rng.standard_normal((sh.num_chunks, sh.feat_dim),
+                                                                   dtype=np.float32)).astype(np.float32)
+    rq = np.random.Generator(np.random.PCG64([seed, 2]))
+    qt = int(rq.integers(0, num_topics))
+    query_x = f32_to_bf16_bits(topics[qt][None, :] + rq.standard_normal((sh.q_len, sh.feat_dim), dtype=np.float32))
+    q = _draw(rq, (sh.q_len, sh.num_q_heads, sh.head_dim), sq)
+    tk = _draw(rq, (sh.tail_len, sh.num_kv_heads, sh.head_dim), sk)
+    tv = _draw(rq, (sh.tail_len, sh.num_kv_heads, sh.head_dim), sv)
+    rs = np.random.Generator(np.random.PCG64([seed, 4]))
+    snk = _draw(rs, (sh.sink_len, sh.num_kv_heads, sh.head_dim), sk)
+    snv = _draw(rs, (sh.sink_len, sh.num_kv_heads, sh.head_dim), sv)
+    return QueryInputs(sh, lens, start, feat, query_x, q, tk, tv, snk, snv, seed=seed, family=family)
+
+
+def make_tokens(n_tokens: int, feat_dim: int, seed=0, offset: float = 0.0) -> np.ndarray:
+    """bf16 bits [n_tokens, feat_dim] of N(offset, 1) token embeddings, PCG64([seed, 5])."""
+    rng = np.random.Generator(np.random.PCG64([seed, 5]))
+    return f32_to_bf16_bits(np.float32(offset) + rng.standard_normal((n_tokens, feat_dim), dtype=np.float32))
+
+
+# Query-side shapes.  Store chunks have 256..1024 retained tokens (25-100 %
+# of a 1024-token chunk); the query is 32 tokens; ur = 32 retrieved chunks.
+QUERY_CONFIGS = {
+    "q_tiny": QueryShape(2, 1, 64, 8, 256, 12, 5, 40, 4, 6, 3),
+    "q_small": QueryShape(8, 2, 128, 16, 512, 40, 16, 200, 16, 16, 8),
+    "q_gqa7": QueryShape(14, 2, 128, 4, 384, 30, 1, 300, 9, 21, 7),
+    "q_7b": QueryShape(28, 4, 128, 64, 3584, 256, 256, 1024, 32, 32, 32),
+    "q_3b": QueryShape(16, 2, 128, 64, 2048, 256, 256, 1024, 32, 32, 32),
 }
