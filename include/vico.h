@@ -138,6 +138,110 @@ int64_t vico_attn_workspace_bytes(int32_t chunk_len, int32_t sink_len, int32_t r
                                   int64_t window, int32_t num_q_heads, int32_t num_kv_heads,
                                   int32_t head_dim, int32_t num_splits);
 
+/* ------------------------------------------------------------------------
+ * Query-side retrieval (Sec. 3, query-time decoding; query rows of Eq. (4)).
+ * The query tokens and each visual chunk's retained tokens are averaged
+ * into one representative feature each; chunks are ranked by the cosine of
+ * the two; only the retrieved chunks' keys and values are visible to the
+ * query tokens.  A typical query: vico_token_mean on the query embeddings,
+ * vico_chunk_scores over the feature table, vico_topk_chunks (which also
+ * writes the store segments), then vico_gather_attn per layer -- no host
+ * synchronisation anywhere in between.
+ * ------------------------------------------------------------------------ */
+
+/*
+ * vico_token_mean -- representative feature: out[c] = (1/L) sum_t x[t][c].
+ *
+ *   x        [num_tokens][feat_dim] bf16, device (LLM input embeddings of a
+ *            chunk's retained tokens, or of the query tokens)
+ *   out      [feat_dim] fp32, device, written
+ * num_tokens >= 1; feat_dim a positive multiple of 8.  fp32 accumulation in a
+ * fixed order (results repeat bit for bit).  x 16-byte, out 16-byte aligned.
+ */
+int vico_token_mean(const void* x, int32_t num_tokens, int32_t feat_dim, float* out, void* stream);
+
+/*
+ * vico_chunk_scores -- s_i = <q, c_i> / (|q| |c_i|) (the retrieval equation
+ * of Sec. 3), fp32.  A zero vector on either side scores 0.
+ *
+ *   query_feat  [feat_dim] fp32, device
+ *   chunk_feat  [num_chunks][feat_dim] fp32, device (one row per stored chunk)
+ *   scores      [num_chunks] fp32, device, written
+ * feat_dim a positive multiple of 8; num_chunks >= 0 (0 is a no-op).
+ */
+int vico_chunk_scores(const float* query_feat, const float* chunk_feat, int32_t num_chunks, int32_t feat_dim,
+                      float* scores, void* stream);
+
+/*
+ * vico_topk_chunks -- the retrieved set: the top_k chunks by score among
+ * those with score >= min_score (pass -INFINITY for plain top-k; a finite
+ * value is the threshold tau_q of the training mask of Eq. (4)).  Equal
+ * scores rank the earlier chunk first; NaN scores are never selected.
+ * The selected chunks are written in ascending chunk order (stream order):
+ *
+ *   out_chunks  [top_k] int32, device: chunk indices, then -1 padding
+ *   out_scores  [top_k] fp32, device: their scores, then -inf padding
+ *   out_count   [1] int32, device: number selected = min(top_k, candidates)
+ *   chunk_start [num_chunks] int64, chunk_len [num_chunks] int32, device:
+ *               the store slot range of every chunk; when both are non-NULL
+ *               the call also writes the segment table of the selection,
+ *   seg_start   [top_k] int64, seg_len [top_k] int32, device (zero padding),
+ *               ready to be passed to vico_gather_attn.
+ * 1 <= top_k <= 2048, num_chunks >= 0.  One work-group; cost grows with
+ * num_chunks (five passes over the scores).
+ */
+int vico_topk_chunks(const float* scores, int32_t num_chunks, int32_t top_k, float min_score,
+                     const int64_t* chunk_start, const int32_t* chunk_len, int32_t* out_chunks,
+                     float* out_scores, int64_t* seg_start, int32_t* seg_len, int32_t* out_count, void* stream);
+
+/*
+ * vico_gather_attn -- attention of short query rows over gathered chunks.
+ *
+ * Attn_q = softmax(Q_q K~^T / sqrt(d)) V~ (Sec. 3) where K~, V~ are built
+ * from the retrieved chunks.  With g = num_q_heads / num_kv_heads, the query
+ * rows are the last q_len of tail_len tail tokens (the query, or the
+ * answer tokens generated so far), and row i of query head h attends to the
+ * keys of KV head h / g in
+ *     sink[0 .. sink_len) ++ store[segment 0] ++ ... ++ store[segment n-1]
+ *                         ++ tail[0 .. tail_len - q_len + i]
+ * where segment s is store slots [seg_start[s], seg_start[s] + seg_len[s]).
+ * q_len = 1 is one decode step; a ring window is passed as one or two
+ * segments of the ring.
+ *
+ *   q              [q_len][num_q_heads][head_dim] bf16, device
+ *   tail_k,tail_v  [tail_len][num_kv_heads][head_dim] bf16, device
+ *   sink_k,sink_v  [sink_len][num_kv_heads][head_dim]; NULL iff sink_len == 0
+ *   store_k,store_v[store_slots][num_kv_heads][head_dim] bf16, device
+ *   seg_start      [num_segments] int64, device (8-byte aligned)
+ *   seg_len        [num_segments] int32, device (4-byte aligned)
+ *   keys_hint      expected total segment length; only sets how the key range
+ *                  is split over work-groups (any value gives the same result)
+ *   out, out_dtype, lse_out, softmax_scale: as for vico_chunk_prefill_attn
+ *                  ([q_len][num_q_heads][head_dim], [num_q_heads][q_len])
+ *   num_splits     0: library's choice; n > 0: key range in n parts (<= 64)
+ *   workspace      at least the bytes vico_gather_plan reports
+ *
+ * The table lives in device memory (vico_topk_chunks writes it), so it is
+ * checked on the device: every segment is clipped to [0, store_slots), and
+ * the parts outside the store are not attended to.  0 <= num_segments <=
+ * 2048; num_segments * store_slots + sink_len + tail_len <= 2^30;
+ * 1 <= q_len <= tail_len.  Arithmetic as for vico_chunk_prefill_attn.
+ */
+int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const void* tail_v, int32_t tail_len,
+                     const void* sink_k, const void* sink_v, int32_t sink_len, const void* store_k,
+                     const void* store_v, int32_t store_slots, const int64_t* seg_start, const int32_t* seg_len,
+                     int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
+                     int32_t head_dim, float softmax_scale, void* out, int32_t out_dtype, float* lse_out,
+                     int32_t num_splits, void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * vico_gather_plan -- key-range parts and workspace of vico_gather_attn for
+ * these arguments (host-only; validates them as the call does).
+ */
+int vico_gather_plan(int32_t q_len, int32_t tail_len, int32_t sink_len, int32_t store_slots,
+                     int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
+                     int32_t head_dim, int32_t num_splits, int32_t* num_splits_out, int64_t* workspace_bytes_out);
+
 /* Static text for a vico_status value. */
 const char* vico_status_str(int status);
 

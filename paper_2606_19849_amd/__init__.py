@@ -4,8 +4,11 @@ The hot path of ViCoStream's bounded visual attention (Sec. 3, "LLM
 Prefilling and Decoding"): each video chunk's retained visual tokens attend
 to a sink prefix, the W newest cached visual tokens and themselves
 (causally) under grouped-query attention; the chunk's K/V then enter a
-ring-buffer cache.  All arithmetic runs in the hand-written HIP kernels of
-libvico.so (C ABI in include/vico.h); this package only marshals arguments.
+ring-buffer cache.  Query-side retrieval (token means, cosine scores, top-k
+chunks) and attention of short queries or decode steps over the retrieved
+chunks complete the query path.  All arithmetic runs in the hand-written HIP
+kernels of libvico.so (C ABI in include/vico.h); this package only marshals
+arguments.
 """
 from ._binding import (
     VICO_DTYPE_BF16,
@@ -19,6 +22,11 @@ from ._binding import (
     vico_attn_workspace_bytes,
     vico_chunk_prefill_attn,
     vico_kv_append,
+    vico_token_mean,
+    vico_chunk_scores,
+    vico_topk_chunks,
+    vico_gather_plan,
+    vico_gather_attn,
 )
 
 __all__ = [
@@ -33,4 +41,9 @@ __all__ = [
     "vico_attn_workspace_bytes",
     "vico_chunk_prefill_attn",
     "vico_kv_append",
+    "vico_token_mean",
+    "vico_chunk_scores",
+    "vico_topk_chunks",
+    "vico_gather_plan",
+    "vico_gather_attn",
 ]

@@ -31,6 +31,13 @@ _SIGNATURES = {
     "vico_attn_plan": (_i32, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32,
                               ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "vico_attn_workspace_bytes": (_i64, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32]),
+    "vico_token_mean": (_i32, [_vp, _i32, _i32, _vp, _vp]),
+    "vico_chunk_scores": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
+    "vico_topk_chunks": (_i32, [_vp, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "vico_gather_plan": (_i32, [_i32, _i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32, _i32,
+                                ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
+    "vico_gather_attn": (_i32, [_vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _i64,
+                                _i32, _i32, _i32, _f32, _vp, _i32, _vp, _i32, _vp, _i64, _vp]),
     "vico_status_str": (ctypes.c_char_p, [_i32]),
     "vico_last_hip_error": (_i32, []),
 }
@@ -148,3 +155,97 @@ def vico_chunk_prefill_attn(q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v,
         int(hist_len), int(window), Hq, Hkv, D, float(softmax_scale), _ptr(out), odt, _ptr(lse),
         int(num_splits), _ptr(workspace), wb, _stream(stream))
     _check(st, "vico_chunk_prefill_attn")
+
+
+def _dev_tensor(name, t, dtype, ndim):
+    if not (t.is_cuda and t.dtype == dtype and t.is_contiguous() and t.dim() == ndim):
+        raise ValueError(f"{name}: expected a contiguous {ndim}-d {dtype} CUDA tensor, got "
+                         f"{tuple(t.shape)} {t.dtype} on {t.device}")
+
+
+def vico_token_mean(x, out, stream=None) -> None:
+    """out[c] = mean over tokens of x[t][c] (vico_token_mean); x bf16 [L, dm], out fp32 [dm]."""
+    _dev_tensor("x", x, torch.bfloat16, 2)
+    _dev_tensor("out", out, torch.float32, 1)
+    L, dm = x.shape
+    if out.shape[0] != dm:
+        raise ValueError("out: expected [feat_dim]")
+    _check(load_library().vico_token_mean(_ptr(x), L, dm, _ptr(out), _stream(stream)), "vico_token_mean")
+
+
+def vico_chunk_scores(query_feat, chunk_feat, scores, stream=None) -> None:
+    """Cosine of the query feature with every chunk feature (vico_chunk_scores)."""
+    _dev_tensor("query_feat", query_feat, torch.float32, 1)
+    _dev_tensor("chunk_feat", chunk_feat, torch.float32, 2)
+    _dev_tensor("scores", scores, torch.float32, 1)
+    N, dm = chunk_feat.shape
+    if query_feat.shape[0] != dm or scores.shape[0] != N:
+        raise ValueError("shape mismatch between query_feat, chunk_feat and scores")
+    _check(load_library().vico_chunk_scores(_ptr(query_feat), _ptr(chunk_feat), N, dm, _ptr(scores),
+                                            _stream(stream)), "vico_chunk_scores")
+
+
+def vico_topk_chunks(scores, top_k: int, out_chunks, out_scores, out_count, min_score: float = float("-inf"),
+                     chunk_start=None, chunk_len=None, seg_start=None, seg_len=None, stream=None) -> None:
+    """Top-k chunks by score with score >= min_score, in stream order (vico_topk_chunks)."""
+    _dev_tensor("scores", scores, torch.float32, 1)
+    _dev_tensor("out_chunks", out_chunks, torch.int32, 1)
+    _dev_tensor("out_scores", out_scores, torch.float32, 1)
+    _dev_tensor("out_count", out_count, torch.int32, 1)
+    if chunk_start is not None:
+        _dev_tensor("chunk_start", chunk_start, torch.int64, 1)
+        _dev_tensor("chunk_len", chunk_len, torch.int32, 1)
+        _dev_tensor("seg_start", seg_start, torch.int64, 1)
+        _dev_tensor("seg_len", seg_len, torch.int32, 1)
+    N = scores.shape[0]
+    for n, t, want in (("out_chunks", out_chunks, top_k), ("out_scores", out_scores, top_k),
+                       ("seg_start", seg_start, top_k), ("seg_len", seg_len, top_k),
+                       ("chunk_start", chunk_start, N), ("chunk_len", chunk_len, N)):
+        if t is not None and t.shape[0] < want:
+            raise ValueError(f"{n}: needs {want} entries")
+    st = load_library().vico_topk_chunks(_ptr(scores), N, int(top_k), float(min_score), _ptr(chunk_start),
+                                         _ptr(chunk_len), _ptr(out_chunks), _ptr(out_scores), _ptr(seg_start),
+                                         _ptr(seg_len), _ptr(out_count), _stream(stream))
+    _check(st, "vico_topk_chunks")
+
+
+def vico_gather_plan(q_len, tail_len, sink_len, store_slots, num_segments, keys_hint, num_q_heads, num_kv_heads,
+                     head_dim, num_splits=0):
+    """(parts, workspace_bytes) of vico_gather_attn for these arguments."""
+    ns, wb = _i32(0), _i64(0)
+    st = load_library().vico_gather_plan(q_len, tail_len, sink_len, store_slots, num_segments, int(keys_hint),
+                                         num_q_heads, num_kv_heads, head_dim, num_splits,
+                                         ctypes.byref(ns), ctypes.byref(wb))
+    _check(st, "vico_gather_plan")
+    return ns.value, wb.value
+
+
+def vico_gather_attn(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out, lse=None,
+                     workspace=None, keys_hint: int = 0, num_splits: int = 0, softmax_scale: float = 0.0,
+                     stream=None) -> None:
+    """Short-query attention over sink ++ store segments ++ causal tail (vico_gather_attn)."""
+    for n, t in (("q", q), ("tail_k", tail_k), ("tail_v", tail_v), ("sink_k", sink_k), ("sink_v", sink_v),
+                 ("store_k", store_k), ("store_v", store_v)):
+        _dev_bf16(n, t)
+    if seg_start is not None:
+        _dev_tensor("seg_start", seg_start, torch.int64, 1)
+        _dev_tensor("seg_len", seg_len, torch.int32, 1)
+    if not (out.is_cuda and out.is_contiguous() and out.dtype in (torch.bfloat16, torch.float32)):
+        raise ValueError("out: expected a contiguous bfloat16 or float32 CUDA tensor")
+    Lq, Hq, D = q.shape
+    T, Hkv = tail_k.shape[0], tail_k.shape[1]
+    S = 0 if sink_k is None else sink_k.shape[0]
+    cap = 0 if store_k is None else store_k.shape[0]
+    n_segs = 0 if seg_start is None else seg_start.shape[0]
+    if tuple(out.shape) != (Lq, Hq, D):
+        raise ValueError(f"out: shape {tuple(out.shape)} != {(Lq, Hq, D)}")
+    if lse is not None and not (lse.is_cuda and lse.dtype == torch.float32 and lse.is_contiguous()
+                                and tuple(lse.shape) == (Hq, Lq)):
+        raise ValueError("lse: expected a contiguous float32 CUDA tensor of shape [num_q_heads, q_len]")
+    wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    odt = VICO_DTYPE_F32 if out.dtype == torch.float32 else VICO_DTYPE_BF16
+    st = load_library().vico_gather_attn(
+        _ptr(q), Lq, _ptr(tail_k), _ptr(tail_v), T, _ptr(sink_k), _ptr(sink_v), S, _ptr(store_k), _ptr(store_v),
+        cap, _ptr(seg_start), _ptr(seg_len), n_segs, int(keys_hint), Hq, Hkv, D, float(softmax_scale), _ptr(out),
+        odt, _ptr(lse), int(num_splits), _ptr(workspace), wb, _stream(stream))
+    _check(st, "vico_gather_attn")

@@ -1,0 +1,417 @@
+// Short-query attention over gathered key segments for gfx950 (CDNA4).
+//
+// Query-side attention of ViCoStream (Sec. 3, query-time decoding; query
+// rows of Eq. (4)): the query tokens attend with softmax(Q K~^T / sqrt(d)) V~
+// over the keys of the retrieved chunks only.  Here the key set of query row
+// i is [sink | store segments, in table order | tail tokens 0 .. T-Lq+i]: the
+// segments are slot ranges of a store of past visual K/V (written on the
+// device by the top-k kernel, or a ring window split at its end), the tail
+// holds the query/answer tokens, of which the query rows are the last Lq.
+// With Lq = 1 this is one decode step.
+//
+// Mapping onto the hardware
+//   * A query head group shares its K/V, so the rows of a work-group are
+//     packed (token, head) pairs of one KV head: packed row r is query token
+//     r / g, head kv*g + r % g.  A decode step (Lq = 1) then still gives g
+//     rows per KV head, and a 32-token query 7*32 = 224 rows: one 256-row
+//     work-group of 8 waves reads each K/V tile once for all of them.
+//   * The tile body (MFMA S^T = K Q^T, online softmax, O^T = V^T P^T with the
+//     transposing LDS read, two 32-key halves) is the one of the chunk
+//     prefill kernel.
+//   * Keys are walked in 64-key tiles, double-buffered in LDS.  A tile inside
+//     the gathered region is loaded straight from HBM into LDS with a slot
+//     resolved per lane (the store is one buffer resource, so the rows of a
+//     tile may come from several segments); tiles inside the sink or the tail
+//     are contiguous; the few tiles that straddle two regions are assembled
+//     synchronously.  Segments are clamped to the store, so no access leaves
+//     it whatever the table holds.
+//   * The segment table (clamped first slots and a prefix sum of lengths) is
+//     built in LDS by every work-group; the device-side table never needs a
+//     host copy.
+//   * Few rows but many keys: the key range is split into parts over the
+//     work-groups, merged by the split-merge kernel of the chunk prefill.
+
+#include <type_traits>
+
+#include "attn_common.h"
+
+namespace vico {
+namespace {
+
+template <int D>
+__global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherArgs a) {
+  constexpr int BN = 64;
+  constexpr int BM = kBlockM;
+  constexpr int NKS = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int UPR = D / 8;
+  constexpr int RBY = D * 2;
+  constexpr int KT = BN * D;
+  constexpr int NW = kThreads / 64;
+  constexpr int NLD = BN * RBY / 1024 / NW;
+  constexpr int RPL = 1024 / RBY;
+  constexpr int SEG_PER_THREAD = kMaxSegments / kThreads;
+  static_assert(NLD * NW * 1024 == BN * RBY, "direct loads cover the tile");
+  static_assert(BM == NW * 32, "one 32-row block per wave");
+  static_assert(SEG_PER_THREAD * kThreads == kMaxSegments, "segment table split");
+  auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
+  auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
+
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds0[KT], k_lds1[KT];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds0[KT], v_lds1[KT];
+  __shared__ int seg_slot[kMaxSegments];
+  __shared__ int seg_pre[kMaxSegments + 1];
+  __shared__ int wave_tot[NW];
+  auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
+    if constexpr (decltype(b)::value == 0) return k_lds0; else return k_lds1;
+  };
+  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
+    if constexpr (decltype(b)::value == 0) return v_lds0; else return v_lds1;
+  };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l32 = lane & 31;
+  const int hh = lane >> 5;
+  const int g = a.Hq / a.Hkv;
+  const int NR = g * a.Lq;                 // packed rows per KV head
+
+  // ---- work item
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int rt = L % a.n_rt;
+  const int part = (L / a.n_rt) % a.parts;
+  const int kv = L / (a.n_rt * a.parts);
+
+  // ---- segment table: clamp every segment to the store, prefix-sum lengths
+  {
+    int len[SEG_PER_THREAD], run = 0;
+#pragma unroll
+    for (int e = 0; e < SEG_PER_THREAD; ++e) {
+      const int i = tid * SEG_PER_THREAD + e;
+      int n = 0, slot = 0;
+      if (i < a.n_segs) {
+        const int64_t st = a.seg_start[i];
+        const int64_t lo = st > 0 ? st : 0;
+        const int64_t en = st + (int64_t)a.seg_len[i];
+        const int64_t hi = en < (int64_t)a.cap ? en : (int64_t)a.cap;
+        if (hi > lo) { n = (int)(hi - lo); slot = (int)lo; }
+      }
+      seg_slot[i] = slot;
+      len[e] = n;
+      run += n;
+    }
+    // inclusive scan of the per-thread totals: within the wave, then across waves
+    int incl = run;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int base = incl - run;
+    for (int w = 0; w < wave; ++w) base += wave_tot[w];
+    if (tid == 0) seg_pre[0] = 0;
+#pragma unroll
+    for (int e = 0; e < SEG_PER_THREAD; ++e) {
+      base += len[e];
+      seg_pre[tid * SEG_PER_THREAD + e + 1] = base;
+    }
+    __syncthreads();
+  }
+  const int S = a.S;
+  const int G = __builtin_amdgcn_readfirstlane(seg_pre[a.n_segs]);   // gathered keys (wave-uniform)
+  const int SG = S + G;
+  const int tail0 = a.T - a.Lq;             // tail tokens before the first query row
+
+  // gathered key j (0 <= j < G) -> store slot
+  auto slot_of = [&](int j) __attribute__((always_inline)) {
+    int lo = 0, hi = a.n_segs - 1;          // last segment with seg_pre[s] <= j
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (seg_pre[mid] <= j) lo = mid; else hi = mid - 1;
+    }
+    return seg_slot[lo] + (j - seg_pre[lo]);
+  };
+
+  // ---- rows of this wave
+  const int wrow0 = rt * BM + wave * 32;
+  const bool wave_active = wrow0 < NR;
+  const int my_row = wrow0 + l32;
+  const int my_tok = min(my_row, NR - 1) / g;
+  const int my_head = kv * g + min(my_row, NR - 1) % g;
+  const int key_lim = SG + tail0 + my_tok;                      // last visible key of this lane's row
+  const int wave_first_lim = SG + tail0 + min(wrow0, NR - 1) / g;
+  const int wave_last_lim = SG + tail0 + min(wrow0 + 31, NR - 1) / g;
+  const int rt_last_tok = (min((rt + 1) * BM, NR) - 1) / g;
+  const int n_tiles = (SG + tail0 + rt_last_tok + 1 + BN - 1) / BN;
+  const int t_lo = (int)((int64_t)n_tiles * part / a.parts);
+  const int t_hi = (int)((int64_t)n_tiles * (part + 1) / a.parts);
+
+  bf16x8 qf[NKS];
+  {
+    const uint16_t* qp = a.q + ((int64_t)my_tok * a.Hq + my_head) * D + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const u32x4 v = (my_row < NR) ? *(const u32x4*)(qp + ks * 16) : u32x4{0u, 0u, 0u, 0u};
+      qf[ks] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  // ---- tile loader (see the chunk prefill kernel for the LDS swizzles)
+  const int rbytes = a.Hkv * D * 2;
+  const rsrc_t rs_sk = make_rsrc(a.sink_k, S * rbytes), rs_sv = make_rsrc(a.sink_v, S * rbytes);
+  const rsrc_t rs_gk = make_rsrc(a.store_k, a.cap * rbytes), rs_gv = make_rsrc(a.store_v, a.cap * rbytes);
+  const rsrc_t rs_tk = make_rsrc(a.tail_k, a.T * rbytes), rs_tv = make_rsrc(a.tail_v, a.T * rbytes);
+  int ld_row[NLD];
+  uint32_t ld_ck[NLD], ld_cv[NLD];
+#pragma unroll
+  for (int n = 0; n < NLD; ++n) {
+    const int r = wave * (BN / NW) + n * RPL + lane / UPR;
+    const int pu = lane % UPR;
+    ld_row[n] = r;
+    ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ fk(r)) * 16);
+    ld_cv[n] = (uint32_t)(kv * D * 2 + (pu ^ fv(r)) * 16);
+  }
+
+  // tile kind (wave-uniform): 0 sink, 1 gathered, 2 tail (all rows inside); 3 mixed
+  auto tile_mode = [&](int t) __attribute__((always_inline)) {
+    const int k0 = t * BN, k1 = k0 + BN;
+    if (k1 <= S) return 0;
+    if (k0 >= S && k1 <= SG) return 1;
+    if (k0 >= SG && k1 <= SG + a.T) return 2;
+    return 3;
+  };
+  auto load_tile = [&](auto buf, int t) __attribute__((always_inline)) {
+    uint16_t* Ks = kbuf(buf);
+    uint16_t* Vs = vbuf(buf);
+    const int k0 = t * BN;
+    const int mode = tile_mode(t);
+    if (mode != 3) {
+      // select base and size, then build one resource (a select between
+      // resources would not stay in scalar registers)
+      const uint16_t* bk = mode == 0 ? a.sink_k : (mode == 1 ? a.store_k : a.tail_k);
+      const uint16_t* bv = mode == 0 ? a.sink_v : (mode == 1 ? a.store_v : a.tail_v);
+      const int nb = (mode == 0 ? S : (mode == 1 ? a.cap : a.T)) * rbytes;
+      const rsrc_t rk_ = make_rsrc(bk, nb), rv_ = make_rsrc(bv, nb);
+#pragma unroll
+      for (int n = 0; n < NLD; ++n) {
+        const int kk = k0 + ld_row[n];
+        const int row = mode == 0 ? kk : (mode == 1 ? slot_of(kk - S) : kk - SG);
+        const uint32_t rowoff = (uint32_t)row * (uint32_t)rbytes;
+        lds_void* kd = (lds_void*)(Ks + (wave * (BN / NW) + n * RPL) * D);
+        lds_void* vd = (lds_void*)(Vs + (wave * (BN / NW) + n * RPL) * D);
+        load_lds16(rk_, kd, rowoff + ld_ck[n]);
+        load_lds16(rv_, vd, rowoff + ld_cv[n]);
+      }
+      return;
+    }
+#pragma unroll
+    for (int n = 0; n < NLD; ++n) {
+      const int kk = k0 + ld_row[n];
+      const uint32_t o_s = kk < S ? (uint32_t)kk * rbytes : kOutOfRange;
+      const uint32_t o_g = (kk >= S && kk < SG) ? (uint32_t)slot_of(kk - S) * rbytes : kOutOfRange;
+      const uint32_t o_t = kk >= SG ? (uint32_t)(kk - SG) * rbytes : kOutOfRange;   // past T: zero
+      const u32x4 kx = __builtin_amdgcn_raw_buffer_load_b128(rs_sk, o_s + ld_ck[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_gk, o_g + ld_ck[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_tk, o_t + ld_ck[n], 0, 0);
+      const u32x4 vx = __builtin_amdgcn_raw_buffer_load_b128(rs_sv, o_s + ld_cv[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_gv, o_g + ld_cv[n], 0, 0) |
+                       __builtin_amdgcn_raw_buffer_load_b128(rs_tv, o_t + ld_cv[n], 0, 0);
+      const int pos = ld_row[n] * D + (lane % UPR) * 8;
+      *(u32x4*)(Ks + pos) = kx;
+      *(u32x4*)(Vs + pos) = vx;
+    }
+  };
+
+  uint32_t k_rd[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) k_rd[ks] = (uint32_t)(l32 * RBY + (((2 * ks) | hh) ^ fk(l32)) * 16);
+  uint32_t v_rd[NDB];
+  {
+    const int j = (lane & 15) >> 2, q = lane & 3;
+    const int r = (lane >> 5) * 4 + j;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const int u = db * 4 + ((lane >> 4) & 1) * 2 + (q >> 1);
+      v_rd[db] = (uint32_t)(r * RBY + (u ^ fv(r)) * 16 + (q & 1) * 8);
+    }
+  }
+
+  f32x16 o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) o[db] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c = a.scale_log2;
+
+  auto qk_half = [&](const uint16_t* Ks, int h, f32x16& s) __attribute__((always_inline)) {
+    s = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const bf16x8 kf = *(const bf16x8*)((const char*)Ks + h * 32 * RBY + k_rd[ks]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
+    }
+  };
+  auto mask_half = [&](int k0h, f32x16& s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int kk = k0h + 8 * (v >> 2) + hh * 4 + (v & 3);
+      if (kk > key_lim) s[v] = -INFINITY;
+    }
+  };
+  auto max_half = [&](const f32x16& s, float& mx) __attribute__((always_inline)) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) m = fmaxf(m, s[v]);
+    mx = pair_max(m) * c;
+    return mx > m_run + kRescaleThreshold;
+  };
+  auto rescale = [&](bool grow, float mx) __attribute__((always_inline)) {
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = (m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+      m_run = m_new;
+    }
+  };
+  auto exp_half = [&](f32x16& s, bf16x8 (&pf)[2]) __attribute__((always_inline)) {
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    float lsum = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -m_use));
+      s[v] = p;
+      lsum += p;
+    }
+    l_run += lsum;
+#pragma unroll
+    for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[kp][e] = (__bf16)s[kp * 8 + e];
+  };
+  auto pv_half = [&](const uint16_t* Vs, int h, const bf16x8 (&pf)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp) {
+        const char* vp = (const char*)Vs + v_rd[db] + (h * 32 + kp * 16) * RBY;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * RBY));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kp], o[db], 0, 0, 0);
+      }
+  };
+  auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    f32x16 s0, s1;
+    float mx0, mx1;
+    bf16x8 p0[2], p1[2];
+    __builtin_amdgcn_s_setprio(1);
+    qk_half(Ks, 0, s0);
+    __builtin_amdgcn_s_setprio(0);
+    if constexpr (MASK) mask_half(k0, s0);
+    rescale(max_half(s0, mx0), mx0);
+    __builtin_amdgcn_s_setprio(1);
+    qk_half(Ks, 1, s1);
+    exp_half(s0, p0);
+    pv_half(Vs, 0, p0);
+    if constexpr (MASK) mask_half(k0 + 32, s1);
+    const bool grow1 = max_half(s1, mx1);
+    __builtin_amdgcn_s_setprio(0);
+    rescale(grow1, mx1);
+    exp_half(s1, p1);
+    __builtin_amdgcn_s_setprio(1);
+    pv_half(Vs, 1, p1);
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  auto step = [&](auto b, int t) __attribute__((always_inline)) {
+    constexpr int B = decltype(b)::value;
+    if (t + 1 < t_hi) load_tile(std::integral_constant<int, 1 - B>{}, t + 1);
+    const int k0 = t * BN;
+    if (wave_active && k0 <= wave_last_lim) {
+      if (k0 + BN - 1 > wave_first_lim)
+        compute_tile(kbuf(b), vbuf(b), k0, std::true_type{});
+      else
+        compute_tile(kbuf(b), vbuf(b), k0, std::false_type{});
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+  if (t_lo < t_hi) {
+    load_tile(std::integral_constant<int, 0>{}, t_lo);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int t = t_lo; t < t_hi; t += 2) {
+      step(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < t_hi) step(std::integral_constant<int, 1>{}, t + 1);
+    }
+  }
+
+  if (!wave_active || my_row >= NR) return;
+  const float l_tot = pair_sum(l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse2 = l_tot > 0.f ? m_run + __log2f(l_tot) : -INFINITY;
+  const int64_t orow = (int64_t)my_tok * a.Hq + my_head;
+  if (a.parts == 1) {
+    if (a.out_f32) {
+      float* op = (float*)a.out + orow * D + hh * 4;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          *(f32x4*)(op + db * 32 + q4 * 8) = f32x4{o[db][q4 * 4] * inv, o[db][q4 * 4 + 1] * inv,
+                                                   o[db][q4 * 4 + 2] * inv, o[db][q4 * 4 + 3] * inv};
+    } else {
+      __bf16* op = (__bf16*)a.out + orow * D + hh * 4;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          *(bf16x4*)(op + db * 32 + q4 * 8) =
+              bf16x4{(__bf16)(o[db][q4 * 4] * inv), (__bf16)(o[db][q4 * 4 + 1] * inv),
+                     (__bf16)(o[db][q4 * 4 + 2] * inv), (__bf16)(o[db][q4 * 4 + 3] * inv)};
+    }
+    if (a.lse && hh == 0) a.lse[(int64_t)my_head * a.Lq + my_tok] = lse2 * kLn2;
+  } else {
+    // partial result of this key range, in the merge kernel's layout (C = Lq)
+    const int64_t pr = ((int64_t)part * a.Hq + my_head) * a.Lq + my_tok;
+    float* op = a.ws_o + pr * D + hh * 4;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        *(f32x4*)(op + db * 32 + q4 * 8) = f32x4{o[db][q4 * 4] * inv, o[db][q4 * 4 + 1] * inv,
+                                                 o[db][q4 * 4 + 2] * inv, o[db][q4 * 4 + 3] * inv};
+    if (hh == 0) a.ws_lse[pr] = lse2;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gather(const GatherArgs& a, hipStream_t stream) {
+  const int grid = a.n_rt * a.parts * a.Hkv;
+  if (a.D == 128)
+    hipLaunchKernelGGL(attn_gather_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(attn_gather_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || a.parts == 1) return err;
+  AttnArgs m{};
+  m.out = a.out;
+  m.lse = a.lse;
+  m.ws_o = a.ws_o;
+  m.ws_lse = a.ws_lse;
+  m.C = a.Lq;
+  m.Hq = a.Hq;
+  m.Hkv = a.Hkv;
+  m.D = a.D;
+  m.splits = a.parts;
+  m.out_f32 = a.out_f32;
+  return launch_merge(m, stream);
+}
+
+}  // namespace vico

@@ -1,0 +1,237 @@
+// Query-side chunk retrieval for gfx950: representative features, cosine
+// scores and top-k selection (ViCoStream, Sec. 3, query-time decoding).
+//
+//   token_mean_kernel   mean over tokens of a [L][dm] bf16 embedding block,
+//                       fp32 out (a chunk's feature at ingest, or the query's)
+//   chunk_scores_kernel s_i = <q, c_i> / (|q| |c_i|) over the feature table
+//   topk_kernel         the k best chunks with s >= tau_q (ties: smaller
+//                       index), written in stream order together with their
+//                       store segments, for the gathered attention
+//
+// All three are bound by HBM or by launch latency; none of them needs a
+// workspace.  Every reduction runs in a fixed order, so results repeat
+// bit for bit.
+
+#include "attn_common.h"
+
+namespace vico {
+namespace {
+
+constexpr int kMeanThreads = 1024;   // 16 waves split the tokens; 4 columns per lane
+constexpr int kMeanCols = 256;       // columns per work-group
+constexpr int kTopkThreads = 1024;
+
+__global__ __launch_bounds__(kMeanThreads) void token_mean_kernel(const uint16_t* __restrict__ x, int L, int dm,
+                                                                  float* __restrict__ out) {
+  constexpr int NW = kMeanThreads / 64;
+  __shared__ f32x4 part[NW][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.x * kMeanCols + lane * 4;
+  f32x4 acc{0.f, 0.f, 0.f, 0.f};
+  if (col < dm) {
+    const uint16_t* p = x + col;
+    for (int t = wave; t < L; t += NW) {
+      const uint2 v = *(const uint2*)(p + (int64_t)t * dm);
+      acc[0] += __uint_as_float(v.x << 16);
+      acc[1] += __uint_as_float(v.x & 0xFFFF0000u);
+      acc[2] += __uint_as_float(v.y << 16);
+      acc[3] += __uint_as_float(v.y & 0xFFFF0000u);
+    }
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0 && col < dm) {
+    f32x4 s = part[0][lane];
+    for (int w = 1; w < NW; ++w) s += part[w][lane];
+    *(f32x4*)(out + col) = f32x4{s[0] / (float)L, s[1] / (float)L, s[2] / (float)L, s[3] / (float)L};
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// one wave per chunk (grid-stride over chunks)
+__global__ __launch_bounds__(256) void chunk_scores_kernel(const float* __restrict__ qf, const float* __restrict__ cf,
+                                                           int N, int dm, float* __restrict__ scores) {
+  const int lane = threadIdx.x & 63;
+  const int gw = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int nw = (gridDim.x * blockDim.x) >> 6;
+  const int n4 = dm / 4;
+  float qq = 0.f;
+  for (int c = lane; c < n4; c += 64) {
+    const f32x4 q = *(const f32x4*)(qf + 4 * c);
+    qq += q[0] * q[0] + q[1] * q[1] + q[2] * q[2] + q[3] * q[3];
+  }
+  qq = wave_sum(qq);
+  for (int i = gw; i < N; i += nw) {
+    const float* row = cf + (int64_t)i * dm;
+    float dot = 0.f, cc = 0.f;
+    for (int c = lane; c < n4; c += 64) {
+      const f32x4 q = *(const f32x4*)(qf + 4 * c);
+      const f32x4 v = *(const f32x4*)(row + 4 * c);
+      dot += q[0] * v[0] + q[1] * v[1] + q[2] * v[2] + q[3] * v[3];
+      cc += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+    }
+    dot = wave_sum(dot);
+    cc = wave_sum(cc);
+    if (lane == 0) {
+      const float den = sqrtf(cc) * sqrtf(qq);
+      scores[i] = den > 0.f ? dot / den + 0.0f : 0.0f;   // + 0 turns -0 into +0
+    }
+  }
+}
+
+// Order-preserving map of a (non-NaN) float to an unsigned key.
+__device__ __forceinline__ uint32_t order_key(float s) {
+  const uint32_t u = __float_as_uint(s + 0.0f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+struct TopkArgs {
+  const float* scores;
+  int N, k;
+  float min_score;
+  const int64_t* chunk_start;
+  const int32_t* chunk_len;
+  int32_t* out_chunks;
+  float* out_scores;
+  int64_t* seg_start;
+  int32_t* seg_len;
+  int32_t* out_count;
+};
+
+// Exclusive block-wide prefix sum of v (1024 threads); *total gets the sum.
+// `buf` holds one slot per wave; the caller separates successive calls with
+// a barrier (done at the end here).
+__device__ __forceinline__ int block_scan(int v, int* buf, int* total) {
+  constexpr int NW = kTopkThreads / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) buf[wave] = incl;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int t = buf[w];
+    base += w < wave ? t : 0;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + incl - v;
+}
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
+  __shared__ int hist[256];
+  __shared__ int scan_buf[kTopkThreads / 64];
+  __shared__ int sh_bin, sh_remaining;
+  const int tid = threadIdx.x;
+  auto is_cand = [&](float s) __attribute__((always_inline)) { return !isnan(s) && s >= a.min_score; };
+
+  // candidates
+  int cnt = 0;
+  for (int i = tid; i < a.N; i += kTopkThreads) cnt += is_cand(a.scores[i]) ? 1 : 0;
+  int n_cand;
+  block_scan(cnt, scan_buf, &n_cand);
+  const bool take_all = n_cand <= a.k;
+
+  // radix select of the k-th largest key, 8 bits at a time from the top
+  uint32_t prefix = 0, mask = 0;
+  int remaining = a.k;
+  if (!take_all) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int b = tid; b < 256; b += kTopkThreads) hist[b] = 0;
+      __syncthreads();
+      for (int i = tid; i < a.N; i += kTopkThreads) {
+        const float s = a.scores[i];
+        if (!is_cand(s)) continue;
+        const uint32_t key = order_key(s);
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int cum = 0, b = 255;
+        for (; b > 0; --b) {
+          if (cum + hist[b] >= remaining) break;
+          cum += hist[b];
+        }
+        sh_bin = b;
+        sh_remaining = remaining - cum;
+      }
+      __syncthreads();
+      prefix |= (uint32_t)sh_bin << shift;
+      mask |= 255u << shift;
+      remaining = sh_remaining;
+      __syncthreads();
+    }
+  }
+  // prefix = key of the k-th best; keys above it are all taken, and
+  // `remaining` of those equal to it, earliest first
+
+  int taken = 0, eq_seen = 0;
+  for (int i0 = 0; i0 < a.N; i0 += kTopkThreads) {
+    const int i = i0 + tid;
+    const float s = i < a.N ? a.scores[i] : 0.f;
+    const bool cand = i < a.N && is_cand(s);
+    const uint32_t key = cand ? order_key(s) : 0u;
+    const bool gt = cand && (take_all || key > prefix);
+    const bool eq = cand && !take_all && key == prefix;
+    int eq_tot;
+    const int eq_rank = eq_seen + block_scan(eq ? 1 : 0, scan_buf, &eq_tot);
+    const bool sel = gt || (eq && eq_rank < remaining);
+    int sel_tot;
+    const int pos = taken + block_scan(sel ? 1 : 0, scan_buf, &sel_tot);
+    if (sel) {
+      a.out_chunks[pos] = i;
+      a.out_scores[pos] = s;
+      if (a.seg_start) {
+        a.seg_start[pos] = a.chunk_start[i];
+        a.seg_len[pos] = a.chunk_len[i];
+      }
+    }
+    taken += sel_tot;
+    eq_seen += eq_tot;
+  }
+  for (int j = taken + tid; j < a.k; j += kTopkThreads) {
+    a.out_chunks[j] = -1;
+    a.out_scores[j] = -INFINITY;
+    if (a.seg_start) {
+      a.seg_start[j] = 0;
+      a.seg_len[j] = 0;
+    }
+  }
+  if (tid == 0) a.out_count[0] = taken;
+}
+
+}  // namespace
+
+hipError_t launch_token_mean(const uint16_t* x, int L, int dm, float* out, hipStream_t stream) {
+  const int blocks = (dm + kMeanCols - 1) / kMeanCols;
+  hipLaunchKernelGGL(token_mean_kernel, dim3(blocks), dim3(kMeanThreads), 0, stream, x, L, dm, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_scores(const float* qf, const float* cf, int N, int dm, float* scores, hipStream_t stream) {
+  const int waves = N < 4096 ? N : 4096;
+  const int blocks = (waves + 3) / 4;
+  hipLaunchKernelGGL(chunk_scores_kernel, dim3(blocks), dim3(256), 0, stream, qf, cf, N, dm, scores);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk(const float* scores, int N, int k, float min_score, const int64_t* chunk_start,
+                       const int32_t* chunk_len, int32_t* out_chunks, float* out_scores, int64_t* seg_start,
+                       int32_t* seg_len, int32_t* out_count, hipStream_t stream) {
+  TopkArgs a{scores, N, k, min_score, chunk_start, chunk_len, out_chunks, out_scores, seg_start, seg_len, out_count};
+  hipLaunchKernelGGL(topk_kernel, dim3(1), dim3(kTopkThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace vico

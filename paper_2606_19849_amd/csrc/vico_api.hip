@@ -126,6 +126,47 @@ int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int3
   return VICO_OK;
 }
 
+struct GatherShape {
+  int Lq, T, S, cap, n_segs, Hq, Hkv, D, parts, n_rt;
+  int64_t ws_bytes;
+};
+
+// Validates the shape arguments of the gathered attention and plans its
+// key-range parts: enough work-groups to cover the CUs while every part keeps
+// at least four key tiles of the expected key count.
+int check_gather_shape(int32_t Lq, int32_t T, int32_t S, int32_t cap, int32_t n_segs, int64_t hint, int32_t Hq,
+                       int32_t Hkv, int32_t D, int32_t splits, GatherShape* sh) {
+  if (Lq < 0 || T < Lq || S < 0 || cap < 0 || n_segs < 0 || n_segs > vico::kMaxSegments || hint < 0 || splits < 0)
+    return VICO_ERR_INVALID_ARG;
+  if (Hq < 1 || Hkv < 1 || Hq > kMaxHeads || Hq % Hkv != 0) return VICO_ERR_INVALID_ARG;
+  if (D != 64 && D != 128) return VICO_ERR_UNSUPPORTED;
+  if (T > kMaxChunk || S > kMaxChunk) return VICO_ERR_INVALID_ARG;
+  if (int64_t(n_segs) * cap + S + T > kMaxKeys) return VICO_ERR_INVALID_ARG;
+  const int64_t row_bytes = int64_t(Hkv) * D * 2;
+  if (row_bytes * T >= kMaxTensorBytes || row_bytes * S >= kMaxTensorBytes || row_bytes * cap >= kMaxTensorBytes ||
+      int64_t(Lq) * Hq * D * 4 >= kMaxTensorBytes)
+    return VICO_ERR_INVALID_ARG;
+  const int g = Hq / Hkv;
+  sh->Lq = Lq; sh->T = T; sh->S = S; sh->cap = cap; sh->n_segs = n_segs;
+  sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;
+  sh->n_rt = (int)((int64_t(g) * Lq + vico::kBlockM - 1) / vico::kBlockM);
+  const int64_t tiles = (S + std::min<int64_t>(hint, kMaxKeys) + T + vico::kKeyTile - 1) / vico::kKeyTile;
+  int parts = 1;
+  if (splits > 0) {
+    parts = std::min(splits, vico::kMaxGatherParts);
+  } else {
+    const int64_t base = int64_t(Hkv) * std::max(sh->n_rt, 1);
+    while (parts * 2 <= vico::kMaxGatherParts && base * parts * 2 <= int64_t(vico::kNumCUs) * vico::kWgPerCU &&
+           tiles >= 4 * int64_t(parts) * 2)
+      parts *= 2;
+  }
+  sh->parts = parts;
+  sh->ws_bytes = parts > 1 ? align256(int64_t(4) * parts * Hq * Lq * D) + int64_t(4) * parts * Hq * Lq : 0;
+  return VICO_OK;
+}
+
+bool aligned_to(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0; }
+
 int hip_fail(hipError_t e) {
   g_last_hip_error = (int)e;
   return VICO_ERR_HIP;
@@ -259,6 +300,136 @@ int vico_kv_append(const void* k_chunk, const void* v_chunk, int32_t chunk_len, 
   a.p0 = (int)(hist_len % ring_slots);
   a.row_elems = num_kv_heads * head_dim;
   const hipError_t e = vico::launch_append(a, (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+int vico_token_mean(const void* x, int32_t num_tokens, int32_t feat_dim, float* out, void* stream) {
+  if (num_tokens < 1 || feat_dim < 8 || feat_dim % 8 != 0) return VICO_ERR_INVALID_ARG;
+  if (!x || !out) return VICO_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(out)) return VICO_ERR_MISALIGNED;
+  if (overlaps(out, int64_t(feat_dim) * 4, x, int64_t(num_tokens) * feat_dim * 2)) return VICO_ERR_INVALID_ARG;
+  const hipError_t e = vico::launch_token_mean((const uint16_t*)x, num_tokens, feat_dim, out, (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+int vico_chunk_scores(const float* query_feat, const float* chunk_feat, int32_t num_chunks, int32_t feat_dim,
+                      float* scores, void* stream) {
+  if (num_chunks < 0 || feat_dim < 8 || feat_dim % 8 != 0) return VICO_ERR_INVALID_ARG;
+  if (num_chunks == 0) return VICO_OK;
+  if (!query_feat || !chunk_feat || !scores) return VICO_ERR_INVALID_ARG;
+  if (!aligned16(query_feat) || !aligned16(chunk_feat) || !aligned_to(scores, 4)) return VICO_ERR_MISALIGNED;
+  const int64_t fb = int64_t(num_chunks) * feat_dim * 4;
+  if (overlaps(scores, int64_t(num_chunks) * 4, chunk_feat, fb) ||
+      overlaps(scores, int64_t(num_chunks) * 4, query_feat, int64_t(feat_dim) * 4))
+    return VICO_ERR_INVALID_ARG;
+  const hipError_t e = vico::launch_chunk_scores(query_feat, chunk_feat, num_chunks, feat_dim, scores,
+                                                 (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+int vico_topk_chunks(const float* scores, int32_t num_chunks, int32_t top_k, float min_score,
+                     const int64_t* chunk_start, const int32_t* chunk_len, int32_t* out_chunks,
+                     float* out_scores, int64_t* seg_start, int32_t* seg_len, int32_t* out_count, void* stream) {
+  if (num_chunks < 0 || top_k < 1 || top_k > vico::kMaxSegments || isnan(min_score)) return VICO_ERR_INVALID_ARG;
+  if ((num_chunks > 0 && !scores) || !out_chunks || !out_scores || !out_count) return VICO_ERR_INVALID_ARG;
+  const bool segs = chunk_start || chunk_len;
+  if (segs && (!chunk_start || !chunk_len || !seg_start || !seg_len)) return VICO_ERR_INVALID_ARG;
+  if (!aligned_to(scores, 4) || !aligned_to(out_chunks, 4) || !aligned_to(out_scores, 4) ||
+      !aligned_to(out_count, 4) || !aligned_to(chunk_start, 8) || !aligned_to(chunk_len, 4) ||
+      !aligned_to(seg_start, 8) || !aligned_to(seg_len, 4))
+    return VICO_ERR_MISALIGNED;
+  const int64_t kb4 = int64_t(top_k) * 4;
+  const void* outs[] = {out_chunks, out_scores, out_count, segs ? (const void*)seg_start : nullptr,
+                        segs ? (const void*)seg_len : nullptr};
+  const int64_t outb[] = {kb4, kb4, 4, 2 * kb4, kb4};
+  const void* ins[] = {scores, chunk_start, chunk_len};
+  const int64_t inb[] = {int64_t(num_chunks) * 4, int64_t(num_chunks) * 8, int64_t(num_chunks) * 4};
+  for (int i = 0; i < 5; ++i) {
+    if (!outs[i]) continue;
+    for (int j = 0; j < 3; ++j)
+      if (ins[j] && overlaps(outs[i], outb[i], ins[j], inb[j])) return VICO_ERR_INVALID_ARG;
+    for (int j = i + 1; j < 5; ++j)
+      if (outs[j] && overlaps(outs[i], outb[i], outs[j], outb[j])) return VICO_ERR_INVALID_ARG;
+  }
+  const hipError_t e = vico::launch_topk(scores, num_chunks, top_k, min_score, segs ? chunk_start : nullptr,
+                                         chunk_len, out_chunks, out_scores, segs ? seg_start : nullptr, seg_len,
+                                         out_count, (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+int vico_gather_plan(int32_t q_len, int32_t tail_len, int32_t sink_len, int32_t store_slots, int32_t num_segments,
+                     int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                     int32_t num_splits, int32_t* num_splits_out, int64_t* workspace_bytes_out) {
+  GatherShape sh;
+  const int st = check_gather_shape(q_len, tail_len, sink_len, store_slots, num_segments, keys_hint, num_q_heads,
+                                    num_kv_heads, head_dim, num_splits, &sh);
+  if (st != VICO_OK) return st;
+  if (num_splits_out) *num_splits_out = sh.parts;
+  if (workspace_bytes_out) *workspace_bytes_out = sh.ws_bytes;
+  return VICO_OK;
+}
+
+int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const void* tail_v, int32_t tail_len,
+                     const void* sink_k, const void* sink_v, int32_t sink_len, const void* store_k,
+                     const void* store_v, int32_t store_slots, const int64_t* seg_start, const int32_t* seg_len,
+                     int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
+                     int32_t head_dim, float softmax_scale, void* out, int32_t out_dtype, float* lse_out,
+                     int32_t num_splits, void* workspace, int64_t workspace_bytes, void* stream) {
+  GatherShape sh;
+  int st = check_gather_shape(q_len, tail_len, sink_len, store_slots, num_segments, keys_hint, num_q_heads,
+                              num_kv_heads, head_dim, num_splits, &sh);
+  if (st != VICO_OK) return st;
+  if (out_dtype != VICO_DTYPE_BF16 && out_dtype != VICO_DTYPE_F32) return VICO_ERR_UNSUPPORTED;
+  if (isnan(softmax_scale) || isinf(softmax_scale)) return VICO_ERR_INVALID_ARG;
+  if (workspace_bytes < 0) return VICO_ERR_INVALID_ARG;
+  if (q_len == 0) return VICO_OK;
+  if (!q || !tail_k || !tail_v || !out) return VICO_ERR_INVALID_ARG;
+  if (sink_len > 0 && (!sink_k || !sink_v)) return VICO_ERR_INVALID_ARG;
+  if (num_segments > 0 && (!seg_start || !seg_len)) return VICO_ERR_INVALID_ARG;
+  if (num_segments > 0 && store_slots > 0 && (!store_k || !store_v)) return VICO_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, out, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return VICO_ERR_MISALIGNED;
+  if (!aligned_to(seg_start, 8) || !aligned_to(seg_len, 4) || !aligned_to(lse_out, 4)) return VICO_ERR_MISALIGNED;
+  if (sh.ws_bytes > 0 && (!workspace || workspace_bytes < sh.ws_bytes)) return VICO_ERR_WORKSPACE;
+  const int64_t ob = int64_t(q_len) * num_q_heads * head_dim * (out_dtype == VICO_DTYPE_F32 ? 4 : 2);
+  const int64_t row = int64_t(num_kv_heads) * head_dim * 2;
+  const int64_t lb = lse_out ? int64_t(num_q_heads) * q_len * 4 : 0;
+  const void* ins[] = {q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len};
+  const int64_t inb[] = {int64_t(q_len) * num_q_heads * head_dim * 2, row * tail_len, row * tail_len,
+                         row * sink_len, row * sink_len, row * store_slots, row * store_slots,
+                         int64_t(num_segments) * 8, int64_t(num_segments) * 4};
+  for (int i = 0; i < 9; ++i)
+    if (ins[i] && (overlaps(out, ob, ins[i], inb[i]) || overlaps(lse_out, lb, ins[i], inb[i])))
+      return VICO_ERR_INVALID_ARG;
+  if (overlaps(out, ob, lse_out, lb)) return VICO_ERR_INVALID_ARG;
+
+  vico::GatherArgs a{};
+  a.q = (const uint16_t*)q;
+  a.tail_k = (const uint16_t*)tail_k;
+  a.tail_v = (const uint16_t*)tail_v;
+  a.sink_k = (const uint16_t*)sink_k;
+  a.sink_v = (const uint16_t*)sink_v;
+  a.store_k = (const uint16_t*)store_k;
+  a.store_v = (const uint16_t*)store_v;
+  a.seg_start = seg_start;
+  a.seg_len = seg_len;
+  a.out = out;
+  a.lse = lse_out;
+  if (sh.parts > 1) {
+    a.ws_o = (float*)workspace;
+    a.ws_lse = (float*)((char*)workspace + align256(int64_t(4) * sh.parts * sh.Hq * sh.Lq * sh.D));
+  }
+  a.Lq = sh.Lq; a.T = sh.T; a.S = sh.S;
+  a.cap = (store_k && store_v) ? sh.cap : 0;
+  a.n_segs = sh.n_segs;
+  a.Hq = sh.Hq; a.Hkv = sh.Hkv; a.D = sh.D;
+  a.parts = sh.parts;
+  a.n_rt = sh.n_rt;
+  a.out_f32 = out_dtype == VICO_DTYPE_F32;
+  const double scale = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(head_dim));
+  a.scale_log2 = (float)(scale * 1.4426950408889634);
+  const hipError_t e = vico::launch_gather(a, (hipStream_t)stream);
   return e == hipSuccess ? VICO_OK : hip_fail(e);
 }
 

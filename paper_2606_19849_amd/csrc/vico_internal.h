@@ -44,6 +44,31 @@ struct AttnArgs {
   float scale_log2;    // softmax scale * log2(e)
 };
 
+// Short-query attention over gathered key segments: query rows are the last
+// Lq of T tail tokens; keys = sink ++ store segments ++ tail (causal).
+constexpr int kMaxSegments = 2048;   // segment table entries per call
+constexpr int kMaxGatherParts = 64;  // key-range parts per row tile
+struct GatherArgs {
+  const uint16_t* q;        // [Lq][Hq][D]
+  const uint16_t* tail_k;   // [T][Hkv][D]
+  const uint16_t* tail_v;
+  const uint16_t* sink_k;   // [S][Hkv][D]
+  const uint16_t* sink_v;
+  const uint16_t* store_k;  // [cap][Hkv][D]
+  const uint16_t* store_v;
+  const int64_t* seg_start; // [n_segs] first store slot of each segment
+  const int32_t* seg_len;   // [n_segs]
+  void* out;                // [Lq][Hq][D]
+  float* lse;               // [Hq][Lq], may be null
+  float* ws_o;              // [parts][Hq][Lq][D] fp32 when parts > 1
+  float* ws_lse;            // [parts][Hq][Lq] (log2 units)
+  int Lq, T, S, cap, n_segs;
+  int Hq, Hkv, D;
+  int parts, n_rt;          // key-range parts, 256-row tiles of packed (token, head) rows
+  int out_f32;
+  float scale_log2;
+};
+
 struct AppendArgs {
   const uint16_t* kc;
   const uint16_t* vc;
@@ -54,6 +79,14 @@ struct AppendArgs {
 };
 
 hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream);
+// Merge of split key ranges (reads ws_o / ws_lse of `splits` parts, C rows per head).
+hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
+hipError_t launch_token_mean(const uint16_t* x, int L, int dm, float* out, hipStream_t stream);
+hipError_t launch_chunk_scores(const float* qf, const float* cf, int N, int dm, float* scores, hipStream_t stream);
+hipError_t launch_topk(const float* scores, int N, int k, float min_score, const int64_t* chunk_start,
+                       const int32_t* chunk_len, int32_t* out_chunks, float* out_scores, int64_t* seg_start,
+                       int32_t* seg_len, int32_t* out_count, hipStream_t stream);
 
 }  // namespace vico

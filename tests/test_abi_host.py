@@ -14,7 +14,8 @@ B = 0x20000000
 MIS = 0x10008
 
 EXPECTED = {"vico_kv_append", "vico_chunk_prefill_attn", "vico_attn_plan", "vico_attn_workspace_bytes",
-            "vico_status_str", "vico_last_hip_error"}
+            "vico_status_str", "vico_last_hip_error", "vico_token_mean", "vico_chunk_scores", "vico_topk_chunks",
+            "vico_gather_plan", "vico_gather_attn"}
 
 
 def test_header_declares_the_expected_entry_points():
@@ -150,3 +151,114 @@ def test_balanced_plan_needs_enough_key_tiles():
 ])
 def test_append_rejects_bad_arguments(args, status):
     assert lib.vico_kv_append(*args, None) == status
+
+
+# ---------------------------------------------------------------- retrieval entry points
+
+@pytest.mark.parametrize("args,status", [
+    ((A, 0, 64, B), -1),                     # no tokens
+    ((A, 8, 60, B), -1),                     # feat_dim not a multiple of 8
+    ((None, 8, 64, B), -1),
+    ((A, 8, 64, None), -1),
+    ((MIS, 8, 64, B), -4),
+    ((A, 8, 64, B + 4), -4),
+    ((A, 8, 64, A + 16), -1),                # out inside x
+])
+def test_token_mean_rejects_bad_arguments(args, status):
+    assert lib.vico_token_mean(*args, None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    ((A, B, -1, 64, B + 0x100000), -1),
+    ((A, B, 4, 12, B + 0x100000), -1),
+    ((None, B, 4, 64, B + 0x100000), -1),
+    ((A, B, 4, 64, None), -1),
+    ((MIS, B, 4, 64, B + 0x100000), -4),
+    ((A, B, 4, 64, B + 0x100), -1),          # scores inside the feature table
+])
+def test_chunk_scores_rejects_bad_arguments(args, status):
+    assert lib.vico_chunk_scores(*args, None) == status
+
+
+def test_chunk_scores_of_no_chunks_is_a_no_op():
+    assert lib.vico_chunk_scores(A, B, 0, 64, None, None) == 0
+
+
+def _topk(**kw):
+    a = dict(sc=A, N=100, k=8, tau=float("-inf"), cs=A + 0x1000, cl=A + 0x2000, oc=B, os=B + 0x100,
+             ss=B + 0x200, sl=B + 0x300, cnt=B + 0x400)
+    a.update(kw)
+    return lib.vico_topk_chunks(a["sc"], a["N"], a["k"], a["tau"], a["cs"], a["cl"], a["oc"], a["os"], a["ss"],
+                                a["sl"], a["cnt"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=0), -1),
+    (dict(k=2049), -1),
+    (dict(N=-1), -1),
+    (dict(tau=float("nan")), -1),
+    (dict(sc=None), -1),
+    (dict(oc=None), -1),
+    (dict(cnt=None), -1),
+    (dict(cl=None), -1),                     # chunk table given by halves
+    (dict(ss=None), -1),                     # chunk table without a segment output
+    (dict(cs=A + 0x1004), -4),               # int64 table not 8-byte aligned
+    (dict(oc=B + 2), -4),
+    (dict(os=B + 0x10), -1),                 # out_scores overlaps out_chunks
+    (dict(oc=A + 0x40), -1),                 # output inside the scores
+])
+def test_topk_rejects_bad_arguments(kw, status):
+    assert _topk(**kw) == status
+
+
+def _gather(**kw):
+    a = dict(q=A, Lq=4, tk=A + 0x100000, tv=A + 0x200000, T=6, sk=A + 0x300000, sv=A + 0x400000, S=8,
+             gk=A + 0x500000, gv=A + 0x600000, cap=500, ss=A + 0x700000, sl=A + 0x701000, n=3, hint=100,
+             Hq=2, Hkv=1, D=64, scale=0.0, out=B, odt=1, lse=None, splits=0, ws=None, wsb=0)
+    a.update(kw)
+    return lib.vico_gather_attn(a["q"], a["Lq"], a["tk"], a["tv"], a["T"], a["sk"], a["sv"], a["S"], a["gk"],
+                                a["gv"], a["cap"], a["ss"], a["sl"], a["n"], a["hint"], a["Hq"], a["Hkv"], a["D"],
+                                a["scale"], a["out"], a["odt"], a["lse"], a["splits"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=3), -1),                         # fewer tail tokens than query rows
+    (dict(Lq=-1), -1),
+    (dict(n=2049), -1),                      # segment table too long
+    (dict(n=-1), -1),
+    (dict(hint=-1), -1),
+    (dict(Hq=3, Hkv=2), -1),
+    (dict(D=80), -2),
+    (dict(odt=5), -2),
+    (dict(scale=float("inf")), -1),
+    (dict(splits=-1), -1),
+    (dict(q=None), -1),
+    (dict(tk=None), -1),
+    (dict(sk=None), -1),
+    (dict(ss=None), -1),
+    (dict(gk=None), -1),
+    (dict(q=MIS), -4),
+    (dict(ss=A + 0x700004), -4),
+    (dict(sl=A + 0x701002), -4),
+    (dict(out=A + 0x500000), -1),            # output inside the store
+    (dict(lse=A + 0x700000), -1),            # lse over the segment table
+    (dict(n=2048, cap=1 << 20), -1),         # possible gathered keys beyond 2^30
+    (dict(splits=4, Lq=4), -5),              # split without a workspace
+])
+def test_gather_rejects_bad_arguments(kw, status):
+    assert _gather(**kw) == status
+
+
+def test_gather_zero_rows_is_a_no_op():
+    assert _gather(Lq=0) == 0
+
+
+def test_gather_plan_parts():
+    # 7B heads, 32-token query, ~20k gathered keys: 4 KV heads x 64 parts fill the CUs
+    assert vico.vico_gather_plan(32, 32, 64, 200000, 32, 20480, 28, 4, 128)[0] == 64
+    # decode step over a short window: few key tiles, few parts
+    p, wb = vico.vico_gather_plan(1, 1, 0, 256, 2, 256, 2, 1, 64)
+    assert p == 1 and wb == 0
+    p, wb = vico.vico_gather_plan(1, 1, 0, 256, 2, 256, 2, 1, 64, num_splits=3)
+    assert p == 3 and wb == 256 * ((3 * 2 * 1 * 64 * 4 + 255) // 256) + 3 * 2 * 4
+    assert vico.vico_gather_plan(1, 1, 0, 256, 2, 256, 2, 1, 64, num_splits=500)[0] == 64
