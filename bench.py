@@ -11,7 +11,9 @@ timed region.
 Default workload: one Qwen2.5-VL-7B-shaped attention layer -- 28 query /
 4 KV heads, head_dim 128, sink 64, W = R = 16384, chunk 2048 -- the shape
 the >= 50 % of bf16 MFMA peak target is stated on.  `--workload` selects the
-others (3b, full, full_bounded, stream).
+others (3b, full, full_bounded, stream, append, and the query-side path:
+query = retrieval + attention over the retrieved chunks, decode = one
+decode step over them).
 
 Prints one JSON line.  `value` is algorithmic TFLOP/s over whole steps
 (attention + append); `roofline` prices the attention kernel alone from
@@ -34,6 +36,7 @@ PEAK_HBM_GBS = 8000.0
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SRC = {"attn_fwd_kernel<128>": "paper_2606_19849_amd/csrc/attn_fwd.hip",
+              "attn_gather_kernel<128>": "paper_2606_19849_amd/csrc/attn_gather.hip",
               "kv_append_kernel": "paper_2606_19849_amd/csrc/kv_append.hip"}
 
 
@@ -70,6 +73,11 @@ DESCR = {
     "full": "3b heads, full history 65536 + sink 64, chunk 2048 (unbounded control)",
     "full_bounded": "3b heads, history 65536 + sink 64, W=8192, chunk 2048",
     "stream": "3b heads, 64 chunks ragged in [256,1024], sink 64, W=R=8192, attend then append",
+    "query": "qwen2.5-vl-7b query-side path per layer: mean of a 32-token query, cosine over 256 stored chunk "
+             "features (dm 3584), top-32 chunks, attention of 32 query rows over sink 64 + retrieved chunks "
+             "(256..1024 tokens each) + causal query; 28q/4kv, d128; 8 queries in rotation",
+    "decode": "qwen2.5-vl-7b decode step per layer: 1 query row over sink 64 + 32 retrieved chunks + 64 tail "
+              "tokens; 28q/4kv, d128; 8 retrieved sets in rotation",
 }
 
 
@@ -246,6 +254,122 @@ def run_stream_workload(args, torch, vico):
     }
 
 
+def run_query_workload(args, torch, vico):
+    """Query-side path on the 7B shape: retrieval (query mean, cosine scores,
+    top-k with segment table) and attention over the retrieved chunks for one
+    layer (`query`), or one decode step over a retrieved set (`decode`).
+    The store holds 256 chunks (336 MB of K/V, more than the 256 MB
+    last-level cache); 8 queries in rotation read different chunks."""
+    import dataclasses
+    from synth import QUERY_CONFIGS, make_query_inputs
+    decode = args.workload == "decode"
+    base = QUERY_CONFIGS["q_7b"]
+    if decode:
+        base = dataclasses.replace(base, tail_len=64)
+    n_q = 8
+    qis = [make_query_inputs(base, seed=0, query_seed=j) for j in range(n_q)]
+    qi0 = qis[0]
+    sh = qi0.shape
+    Lq = 1 if decode else sh.q_len
+    dev = lambda bits: _dev(torch, bits)
+    k_np, v_np = qi0.store_kv()
+    gk, gv = dev(k_np), dev(v_np)
+    del k_np, v_np
+    sk, sv = dev(qi0.sink_k), dev(qi0.sink_v)
+    feats = torch.from_numpy(qi0.chunk_feat).cuda()
+    cstart = torch.from_numpy(qi0.chunk_start).cuda()
+    clen = torch.from_numpy(qi0.chunk_len.astype(np.int32)).cuda()
+    qs = [dict(x=dev(qi.query_x), q=dev(qi.q)[-Lq:].contiguous(), tk=dev(qi.tail_k), tv=dev(qi.tail_v),
+               ss=torch.empty(sh.top_k, dtype=torch.int64, device="cuda"),
+               sl=torch.empty(sh.top_k, dtype=torch.int32, device="cuda")) for qi in qis]
+    qf = torch.empty(sh.feat_dim, dtype=torch.float32, device="cuda")
+    scores = torch.empty(sh.num_chunks, dtype=torch.float32, device="cuda")
+    oc = torch.empty(sh.top_k, dtype=torch.int32, device="cuda")
+    osc = torch.empty(sh.top_k, dtype=torch.float32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    hint = sh.top_k * (sh.chunk_lo + sh.chunk_hi) // 2
+    parts, wb = vico.vico_gather_plan(Lq, sh.tail_len, sh.sink_len, qi0.store_len, sh.top_k, hint,
+                                      sh.num_q_heads, sh.num_kv_heads, sh.head_dim)
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+    out = torch.empty((Lq, sh.num_q_heads, sh.head_dim), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((sh.num_q_heads, Lq), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def retrieve(d):
+        vico.vico_token_mean(d["x"], qf, stream=stream)
+        vico.vico_chunk_scores(qf, feats, scores, stream=stream)
+        vico.vico_topk_chunks(scores, sh.top_k, oc, osc, cnt, chunk_start=cstart, chunk_len=clen,
+                              seg_start=d["ss"], seg_len=d["sl"], stream=stream)
+
+    def attend(d):
+        vico.vico_gather_attn(d["q"], d["tk"], d["tv"], sk, sv, gk, gv, d["ss"], d["sl"], out, lse=lse,
+                              workspace=ws, keys_hint=hint, stream=stream)
+
+    # every query's segment table once (decode steps reuse them)
+    for d in qs:
+        retrieve(d)
+    torch.cuda.synchronize()
+    gathered = [int(d["sl"].sum().item()) for d in qs]
+
+    def step(j, events=None):
+        d = qs[j % n_q]
+        if events:
+            events[0].record(stream)
+        if not decode:
+            retrieve(d)
+        if events:
+            events[1].record(stream)
+        attend(d)
+        if events:
+            events[2].record(stream)
+
+    for j in range(args.warmup):
+        step(j)
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for j in range(args.steps):
+        step(args.warmup + j, ev[j])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ret_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    att_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    Hq, Hkv, D, S, T = sh.num_q_heads, sh.num_kv_heads, sh.head_dim, sh.sink_len, sh.tail_len
+    G = np.array([gathered[(args.warmup + j) % n_q] for j in range(args.steps)], dtype=np.float64)
+    keys = S + G + T
+    kv_bytes = keys * Hkv * D * 2 * 2
+    bytes_ = kv_bytes + Lq * Hq * D * 2 * 2 + Hq * Lq * 4            # + Q, O (bf16), LSE
+    rows = T - Lq + np.arange(Lq) + 1                                   # visible tail keys per query row
+    flops = np.array([4.0 * Hq * D * float(np.sum(S + g + rows)) for g in G])
+    gbs = float(np.mean(bytes_ / (att_ms * 1e-3)) / 1e9)
+    tfl = float(np.mean(flops / (att_ms * 1e-3)) / 1e12)
+    t_hbm = bytes_.mean() / (PEAK_HBM_GBS * 1e9)
+    t_mfma = flops.mean() / (PEAK_BF16_TFLOPS * 1e12)
+    res = {
+        "metric": ("decode-step attention per layer" if decode else
+                   "query-side retrieval + gathered attention per layer (TTFT building block)"),
+        "value": round(args.steps / elapsed, 1), "unit": "steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": DESCR[args.workload], "q_rows": Lq, "tail": T, "top_k": sh.top_k,
+                   "stored_chunks": sh.num_chunks, "store_tokens": qi0.store_len, "parts": parts,
+                   "gathered_keys_mean": float(G.mean())},
+        "retrieval_us_mean": None if decode else round(float(ret_ms.mean()) * 1e3, 2),
+        "attn_us_mean": round(float(att_ms.mean()) * 1e3, 2),
+        "attn_us_median": round(float(np.median(att_ms)) * 1e3, 2),
+        "attn_tflops": round(tfl, 2),
+        "roofline": {"bound": "hbm" if t_hbm >= t_mfma else "mfma",
+                     "achieved": round(gbs, 1) if t_hbm >= t_mfma else round(tfl, 2),
+                     "peak": PEAK_HBM_GBS if t_hbm >= t_mfma else PEAK_BF16_TFLOPS,
+                     "unit": "GB/s" if t_hbm >= t_mfma else "TFLOP/s",
+                     "frac": round(gbs / PEAK_HBM_GBS if t_hbm >= t_mfma else tfl / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic("attn_gather_kernel<128>", args.workload),
+                     "kernel": "attn_gather_kernel<128> (+ split merge)",
+                     "bytes_per_launch_mean": float(bytes_.mean()), "flops_per_launch_mean": float(flops.mean())},
+    }
+    return res
+
+
 def run_append_workload(args, torch, vico):
     """Ring append at capacity (chunk = ring = 16384 tokens of the 7B shape): HBM roofline
     of the append kernel, which is also a plain copy of known size."""
@@ -290,7 +414,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append"])
+    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append", "query", "decode"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--traffic-bytes", type=float, default=None,
@@ -311,6 +435,8 @@ def main():
         res = run_stream_workload(args, torch, vico)
     elif args.workload == "append":
         res = run_append_workload(args, torch, vico)
+    elif args.workload in ("query", "decode"):
+        res = run_query_workload(args, torch, vico)
     else:
         res = run_chunk_workload(args, torch, vico)
     print(json.dumps(res), flush=True)

@@ -52,4 +52,15 @@ __device__ __forceinline__ void load_lds16(rsrc_t r, lds_void* lds, uint32_t vof
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voffset, 0, 0, 0);
 }
 
+// s_waitcnt immediate: vmcnt(n), lgkmcnt(0), expcnt not waited for.
+constexpr uint32_t waitcnt_vm_lgkm0(uint32_t n) { return 0x0070u | n; }
+
+// Work-group barrier that waits for nothing by itself.  __syncthreads()
+// carries a work-group release fence, and the compiler implements that by
+// waiting for every outstanding load, including direct-to-LDS prefetches that
+// are meant to stay in flight across the barrier.  Callers wait for what they
+// need with s_waitcnt first; the "memory" clobber keeps the compiler from
+// moving memory accesses across the barrier.
+__device__ __forceinline__ void barrier_keep_loads() { asm volatile("s_barrier" ::: "memory"); }
+
 }  // namespace vico

@@ -522,42 +522,6 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   }
 }
 
-// Merge of split key ranges: O = sum_s 2^(lse_s - lse) O_s, lse = log2 sum_s 2^lse_s.
-template <int D>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int NQ = D / 4;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)a.Hq * a.C * NQ;
-  if (idx >= total) return;
-  const int dq = (int)(idx % NQ);
-  const int64_t hr = idx / NQ;
-  const int row = (int)(hr % a.C);
-  const int h = (int)(hr / a.C);
-  const int64_t stride_s = (int64_t)a.Hq * a.C;
-  float mx = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, a.ws_lse[s * stride_s + hr]);
-  const float m_use = (mx == -INFINITY) ? 0.f : mx;
-  f32x4 acc{0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    const float ls = a.ws_lse[s * stride_s + hr];
-    if (ls == -INFINITY) continue;      // empty part: its O slot may never have been written
-    const float w = __builtin_amdgcn_exp2f(ls - m_use);
-    const f32x4 v = *(const f32x4*)(a.ws_o + (s * stride_s + hr) * D + dq * 4);
-    wsum += w;
-    acc += w * v;
-  }
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  acc *= inv;
-  const int64_t oo = ((int64_t)row * a.Hq + h) * D + dq * 4;
-  if (a.out_f32) {
-    *(f32x4*)((float*)a.out + oo) = acc;
-  } else {
-    *(bf16x4*)((__bf16*)a.out + oo) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
-  }
-  if (dq == 0 && a.lse) a.lse[(int64_t)h * a.C + row] = wsum > 0.f ? (m_use + __log2f(wsum)) * kLn2 : -INFINITY;
-}
-
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream) {
@@ -570,16 +534,6 @@ hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream) {
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || a.splits == 1) return err;
   return launch_merge(a, stream);
-}
-
-hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
-  const int64_t total = (int64_t)a.Hq * a.C * (a.D / 4);
-  const int blocks = (int)((total + 255) / 256);
-  if (a.D == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(blocks), dim3(256), 0, stream, a);
-  return hipGetLastError();
 }
 
 }  // namespace vico

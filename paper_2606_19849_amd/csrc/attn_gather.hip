@@ -57,17 +57,24 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
   auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
   auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
 
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds0[KT], k_lds1[KT];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds0[KT], v_lds1[KT];
+  // NBUF K/V buffers, tile t in buffer t mod NBUF, loaded NBUF-1 tiles ahead:
+  // this kernel is bound by HBM, so three tiles stay in flight per work-group.
+  // Separate arrays let the compiler see that reads of one buffer do not wait
+  // for the direct loads landing in another.
+  // (One array per buffer, K then V: the compiler tells apart only a few LDS
+  // objects with direct loads in flight, and treats the rest as one.)
+  constexpr int NBUF = 4;
+  __shared__ __attribute__((aligned(16))) uint16_t kv_lds0[2 * KT], kv_lds1[2 * KT], kv_lds2[2 * KT],
+      kv_lds3[2 * KT];
   __shared__ int seg_slot[kMaxSegments];
   __shared__ int seg_pre[kMaxSegments + 1];
   __shared__ int wave_tot[NW];
   auto kbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
-    if constexpr (decltype(b)::value == 0) return k_lds0; else return k_lds1;
+    constexpr int B = decltype(b)::value;
+    if constexpr (B == 0) return kv_lds0; else if constexpr (B == 1) return kv_lds1;
+    else if constexpr (B == 2) return kv_lds2; else return kv_lds3;
   };
-  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* {
-    if constexpr (decltype(b)::value == 0) return v_lds0; else return v_lds1;
-  };
+  auto vbuf = [&](auto b) __attribute__((always_inline)) -> uint16_t* { return kbuf(b) + KT; };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -82,6 +89,26 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
   const int rt = L % a.n_rt;
   const int part = (L / a.n_rt) % a.parts;
   const int kv = L / (a.n_rt * a.parts);
+
+  // ---- this lane's packed row
+  const int wrow0 = rt * BM + wave * 32;
+  const bool wave_active = wrow0 < NR;
+  const int my_row = wrow0 + l32;
+  const int my_tok = min(my_row, NR - 1) / g;
+  const int my_head = kv * g + min(my_row, NR - 1) % g;
+
+  // Q rows as MFMA B fragments.  The loads are unconditional: rows past the
+  // end repeat the last row (the clamped address) and are never stored, and
+  // a row's softmax only mixes the two lanes of that row.  (Loads under
+  // branches, or a later fix-up of their values, leave the compiler unsure
+  // whether they completed, and it then waits for every load in flight.)
+  // Issued first, so that the wait for the segment table covers them.
+  bf16x8 qf[NKS];
+  {
+    const uint16_t* qp = a.q + ((int64_t)my_tok * a.Hq + my_head) * D + hh * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + ks * 16));
+  }
 
   // ---- segment table: clamp every segment to the store, prefix-sum lengths
   {
@@ -118,6 +145,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
       base += len[e];
       seg_pre[tid * SEG_PER_THREAD + e + 1] = base;
     }
+    // Q and the table have landed by now; saying so keeps the compiler from
+    // waiting for them again, i.e. for every tile load in flight, in the loop.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
     __syncthreads();
   }
   const int S = a.S;
@@ -125,22 +155,24 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
   const int SG = S + G;
   const int tail0 = a.T - a.Lq;             // tail tokens before the first query row
 
-  // gathered key j (0 <= j < G) -> store slot
+  // Gathered key j (0 <= j < G) -> store slot.  Tiles are loaded in key
+  // order, so the segment of a tile's first gathered key is found by walking
+  // on from the previous tile's (seg_cur, wave-uniform); each lane then walks
+  // on from there to its own row's segment (rarely more than one step).
+  // Both walks stop below n_segs because seg_pre[n_segs] = G and the index
+  // is kept in [seg_pre[seg_cur], G).
+  int seg_cur = 0;
+  auto seg_advance = [&](int j0) __attribute__((always_inline)) {   // caller: 0 <= j0 < G
+    while (seg_pre[seg_cur + 1] <= j0) ++seg_cur;
+  };
   auto slot_of = [&](int j) __attribute__((always_inline)) {
-    int lo = 0, hi = a.n_segs - 1;          // last segment with seg_pre[s] <= j
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (seg_pre[mid] <= j) lo = mid; else hi = mid - 1;
-    }
-    return seg_slot[lo] + (j - seg_pre[lo]);
+    j = min(max(j, seg_pre[seg_cur]), G - 1);
+    int s = seg_cur;
+    while (seg_pre[s + 1] <= j) ++s;
+    return seg_slot[s] + (j - seg_pre[s]);
   };
 
-  // ---- rows of this wave
-  const int wrow0 = rt * BM + wave * 32;
-  const bool wave_active = wrow0 < NR;
-  const int my_row = wrow0 + l32;
-  const int my_tok = min(my_row, NR - 1) / g;
-  const int my_head = kv * g + min(my_row, NR - 1) % g;
+  // ---- key limits of this wave's rows
   const int key_lim = SG + tail0 + my_tok;                      // last visible key of this lane's row
   const int wave_first_lim = SG + tail0 + min(wrow0, NR - 1) / g;
   const int wave_last_lim = SG + tail0 + min(wrow0 + 31, NR - 1) / g;
@@ -148,16 +180,6 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
   const int n_tiles = (SG + tail0 + rt_last_tok + 1 + BN - 1) / BN;
   const int t_lo = (int)((int64_t)n_tiles * part / a.parts);
   const int t_hi = (int)((int64_t)n_tiles * (part + 1) / a.parts);
-
-  bf16x8 qf[NKS];
-  {
-    const uint16_t* qp = a.q + ((int64_t)my_tok * a.Hq + my_head) * D + hh * 8;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const u32x4 v = (my_row < NR) ? *(const u32x4*)(qp + ks * 16) : u32x4{0u, 0u, 0u, 0u};
-      qf[ks] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
 
   // ---- tile loader (see the chunk prefill kernel for the LDS swizzles)
   const int rbytes = a.Hkv * D * 2;
@@ -183,11 +205,14 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
     if (k0 >= SG && k1 <= SG + a.T) return 2;
     return 3;
   };
+  // returns true when the tile went out as asynchronous direct loads
   auto load_tile = [&](auto buf, int t) __attribute__((always_inline)) {
     uint16_t* Ks = kbuf(buf);
     uint16_t* Vs = vbuf(buf);
     const int k0 = t * BN;
     const int mode = tile_mode(t);
+    const int j0 = max(k0 - S, 0);
+    if (k0 + BN > S && j0 < G) seg_advance(j0);
     if (mode != 3) {
       // select base and size, then build one resource (a select between
       // resources would not stay in scalar registers)
@@ -205,7 +230,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
         load_lds16(rk_, kd, rowoff + ld_ck[n]);
         load_lds16(rv_, vd, rowoff + ld_cv[n]);
       }
-      return;
+      return true;
     }
 #pragma unroll
     for (int n = 0; n < NLD; ++n) {
@@ -223,6 +248,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
       *(u32x4*)(Ks + pos) = kx;
       *(u32x4*)(Vs + pos) = vx;
     }
+    return false;
   };
 
   uint32_t k_rd[NKS];
@@ -328,9 +354,19 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
     __builtin_amdgcn_s_setprio(0);
   };
 
-  auto step = [&](auto b, int t) __attribute__((always_inline)) {
+  // Key loop.  Step t computes tile t while tiles t+1 .. t+NBUF-1 load; it
+  // then waits for tile t+1 only: the direct loads of the newer tiles (each
+  // wave issues 2*NLD per asynchronous tile, and loads complete in order)
+  // may stay in flight.  `newer_async` = whether tile t+2 went out async.
+  // (lgkmcnt(0) too: the synchronous tile path writes LDS with ds_write)
+  constexpr uint32_t kWait0 = waitcnt_vm_lgkm0(0);
+  constexpr uint32_t kWait1 = waitcnt_vm_lgkm0(2 * NLD);
+  constexpr uint32_t kWait2 = waitcnt_vm_lgkm0(4 * NLD);
+  static_assert(4 * NLD < 16, "vmcnt immediate");
+  auto step = [&](auto b, int t, bool& newer_async) __attribute__((always_inline)) {
     constexpr int B = decltype(b)::value;
-    if (t + 1 < t_hi) load_tile(std::integral_constant<int, 1 - B>{}, t + 1);
+    bool an = false;
+    if (t + NBUF - 1 < t_hi) an = load_tile(std::integral_constant<int, (B + NBUF - 1) % NBUF>{}, t + NBUF - 1);
     const int k0 = t * BN;
     if (wave_active && k0 <= wave_last_lim) {
       if (k0 + BN - 1 > wave_first_lim)
@@ -338,16 +374,29 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
       else
         compute_tile(kbuf(b), vbuf(b), k0, std::false_type{});
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    const int n_newer = (newer_async ? 1 : 0) + (an ? 1 : 0);
+    if (n_newer == 2) __builtin_amdgcn_s_waitcnt(kWait2);
+    else if (n_newer == 1) __builtin_amdgcn_s_waitcnt(kWait1);
+    else __builtin_amdgcn_s_waitcnt(kWait0);
+    barrier_keep_loads();
+    newer_async = an;
   };
   if (t_lo < t_hi) {
+    static_assert(NBUF == 4, "prologue loads three tiles");
     load_tile(std::integral_constant<int, 0>{}, t_lo);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    for (int t = t_lo; t < t_hi; t += 2) {
-      step(std::integral_constant<int, 0>{}, t);
-      if (t + 1 < t_hi) step(std::integral_constant<int, 1>{}, t + 1);
+    const bool a1 = t_lo + 1 < t_hi && load_tile(std::integral_constant<int, 1>{}, t_lo + 1);
+    const bool a2 = t_lo + 2 < t_hi && load_tile(std::integral_constant<int, 2>{}, t_lo + 2);
+    const int n_newer = (a1 ? 1 : 0) + (a2 ? 1 : 0);
+    if (n_newer == 2) __builtin_amdgcn_s_waitcnt(kWait2);
+    else if (n_newer == 1) __builtin_amdgcn_s_waitcnt(kWait1);
+    else __builtin_amdgcn_s_waitcnt(kWait0);
+    barrier_keep_loads();
+    bool newer_async = a2;
+    for (int t = t_lo; t < t_hi; t += NBUF) {
+      step(std::integral_constant<int, 0>{}, t, newer_async);
+      if (t + 1 < t_hi) step(std::integral_constant<int, 1>{}, t + 1, newer_async);
+      if (t + 2 < t_hi) step(std::integral_constant<int, 2>{}, t + 2, newer_async);
+      if (t + 3 < t_hi) step(std::integral_constant<int, 3>{}, t + 3, newer_async);
     }
   }
 

@@ -1,0 +1,151 @@
+// Log-sum-exp merge of attention over split key ranges, for gfx950.
+//
+// Each part s of a row's key range left a normalised partial output O_s and
+// its log2-sum-exp lse_s in the workspace; the whole-range result is
+//     lse = log2 sum_s 2^lse_s,   O = sum_s 2^(lse_s - lse) O_s
+// (a part that saw no key of the row carries lse_s = -inf and is skipped;
+// its O_s slot may never have been written).
+//
+// Few parts (up to 8, the chunk prefill splits) over many rows: one thread
+// per 4 columns of a row walks the parts.  Many parts (up to 64, short
+// queries): a thread walking them one by one is bound by load latency, so a
+// work-group of 256 threads takes RPB rows, and for each row PG groups of
+// threads take every PG-th part and D/4 threads the 4-float columns -- all
+// loads of a row are then in flight together.  The part weights come from
+// one wave-wide max and sum over the parts (lane = part).
+
+#include "attn_common.h"
+
+namespace vico {
+namespace {
+
+constexpr int kMergeThreads = 256;
+constexpr int kFewParts = 8;     // up to here one thread per (row, 4 columns) walks the parts
+
+// Few parts, many rows (chunk prefill splits): one thread per (head, row,
+// 4-column group) walks the parts; neighbouring threads read neighbouring
+// columns, so every load is a full coalesced row.
+template <int D>
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs a) {
+  constexpr int NQ = D / 4;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n_rows = (int64_t)a.Hq * a.C;
+  if (idx >= n_rows * NQ) return;
+  const int dq = (int)(idx % NQ);
+  const int64_t hr = idx / NQ;
+  float mx = -INFINITY;
+  for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, a.ws_lse[s * n_rows + hr]);
+  const float m_use = (mx == -INFINITY) ? 0.f : mx;
+  f32x4 acc{0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  for (int s = 0; s < a.splits; ++s) {
+    const float ls = a.ws_lse[s * n_rows + hr];
+    if (ls == -INFINITY) continue;      // empty part: its O slot may never have been written
+    const float w = __builtin_amdgcn_exp2f(ls - m_use);
+    wsum += w;
+    acc += w * *(const f32x4*)(a.ws_o + (s * n_rows + hr) * D + dq * 4);
+  }
+  acc *= wsum > 0.f ? 1.f / wsum : 0.f;
+  const int row = (int)(hr % a.C);
+  const int h = (int)(hr / a.C);
+  const int64_t oo = ((int64_t)row * a.Hq + h) * D + dq * 4;
+  if (a.out_f32) {
+    *(f32x4*)((float*)a.out + oo) = acc;
+  } else {
+    *(bf16x4*)((__bf16*)a.out + oo) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+  }
+  if (dq == 0 && a.lse) a.lse[(int64_t)h * a.C + row] = wsum > 0.f ? (m_use + __log2f(wsum)) * kLn2 : -INFINITY;
+}
+
+// Many parts (short queries): see the file comment.
+
+template <int D>
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a, int PG, int RPB) {
+  constexpr int NQ = D / 4;                       // float4 columns per row
+  __shared__ float w_s[kMergeThreads / NQ][64];   // per row of the block: part weights
+  __shared__ float inv_s[kMergeThreads / NQ];
+  __shared__ float lse_s[kMergeThreads / NQ];
+  __shared__ f32x4 acc_s[kMergeThreads];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t n_rows = (int64_t)a.Hq * a.C;
+  const int64_t stride = n_rows;                  // parts are [splits][Hq][C]
+  const int64_t r0 = (int64_t)blockIdx.x * RPB;
+
+  // weights of every row of the block: wave w takes rows w, w+4, ...
+  for (int r = wave; r < RPB; r += kMergeThreads / 64) {
+    const int64_t hr = r0 + r;
+    float ls = -INFINITY;
+    if (hr < n_rows && lane < a.splits) ls = a.ws_lse[lane * stride + hr];
+    float mx = ls;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    const float m_use = (mx == -INFINITY) ? 0.f : mx;
+    const float w = (ls == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ls - m_use);
+    float sum = w;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+    w_s[r][lane] = w;
+    if (lane == 0) {
+      inv_s[r] = sum > 0.f ? 1.f / sum : 0.f;
+      lse_s[r] = sum > 0.f ? (m_use + __log2f(sum)) * kLn2 : -INFINITY;
+    }
+  }
+  __syncthreads();
+
+  // thread = (row r, part group pg, column dq)
+  const int dq = tid % NQ;
+  const int pg = (tid / NQ) % PG;
+  const int r = tid / (NQ * PG);
+  const int64_t hr = r0 + r;
+  f32x4 acc{0.f, 0.f, 0.f, 0.f};
+  if (r < RPB && hr < n_rows) {
+    for (int p = pg; p < a.splits; p += PG) {
+      const float w = w_s[r][p];
+      const f32x4 v = *(const f32x4*)(a.ws_o + (p * stride + hr) * D + dq * 4);
+      acc += w != 0.f ? w * v : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  acc_s[tid] = acc;
+  __syncthreads();
+  if (pg != 0 || r >= RPB || hr >= n_rows) return;
+  for (int g = 1; g < PG; ++g) acc += acc_s[tid + g * NQ];
+  acc *= inv_s[r];
+  const int row = (int)(hr % a.C);
+  const int h = (int)(hr / a.C);
+  const int64_t oo = ((int64_t)row * a.Hq + h) * D + dq * 4;
+  if (a.out_f32) {
+    *(f32x4*)((float*)a.out + oo) = acc;
+  } else {
+    *(bf16x4*)((__bf16*)a.out + oo) = bf16x4{(__bf16)acc[0], (__bf16)acc[1], (__bf16)acc[2], (__bf16)acc[3]};
+  }
+  if (dq == 0 && a.lse) a.lse[(int64_t)h * a.C + row] = lse_s[r];
+}
+
+}  // namespace
+
+hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
+  if (a.splits < 1 || a.splits > 64) return hipErrorInvalidValue;   // one wave holds the part weights
+  const int64_t rows = (int64_t)a.Hq * a.C;
+  if (a.splits <= kFewParts) {
+    const int blocks = (int)((rows * (a.D / 4) + kMergeThreads - 1) / kMergeThreads);
+    if (a.D == 128)
+      hipLaunchKernelGGL(attn_merge_rows_kernel<128>, dim3(blocks), dim3(kMergeThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(attn_merge_rows_kernel<64>, dim3(blocks), dim3(kMergeThreads), 0, stream, a);
+    return hipGetLastError();
+  }
+  // part groups: the parts rounded up to a power of two, at most what one row's
+  // columns leave of the 256 threads; the remaining threads take more rows
+  const int nq = a.D / 4;
+  int pg = 1;
+  while (pg < a.splits && pg * 2 * nq <= kMergeThreads) pg *= 2;
+  const int rpb = kMergeThreads / (nq * pg);
+  const int blocks = (int)((rows + rpb - 1) / rpb);
+  if (a.D == 128)
+    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(blocks), dim3(kMergeThreads), 0, stream, a, pg, rpb);
+  else
+    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(blocks), dim3(kMergeThreads), 0, stream, a, pg, rpb);
+  return hipGetLastError();
+}
+
+}  // namespace vico

@@ -20,6 +20,7 @@ namespace {
 constexpr int kMeanThreads = 1024;   // 16 waves split the tokens; 4 columns per lane
 constexpr int kMeanCols = 256;       // columns per work-group
 constexpr int kTopkThreads = 1024;
+constexpr int kTopkRegKeys = 8;      // scores kept in registers per thread (N <= 8192 read once)
 
 __global__ __launch_bounds__(kMeanThreads) void token_mean_kernel(const uint16_t* __restrict__ x, int L, int dm,
                                                                   float* __restrict__ out) {
@@ -69,6 +70,7 @@ __global__ __launch_bounds__(256) void chunk_scores_kernel(const float* __restri
   for (int i = gw; i < N; i += nw) {
     const float* row = cf + (int64_t)i * dm;
     float dot = 0.f, cc = 0.f;
+#pragma unroll 4
     for (int c = lane; c < n4; c += 64) {
       const f32x4 q = *(const f32x4*)(qf + 4 * c);
       const f32x4 v = *(const f32x4*)(row + 4 * c);
@@ -130,15 +132,32 @@ __device__ __forceinline__ int block_scan(int v, int* buf, int* total) {
 }
 
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
+  constexpr int NR = kTopkRegKeys;
   __shared__ int hist[256];
   __shared__ int scan_buf[kTopkThreads / 64];
   __shared__ int sh_bin, sh_remaining;
-  const int tid = threadIdx.x;
-  auto is_cand = [&](float s) __attribute__((always_inline)) { return !isnan(s) && s >= a.min_score; };
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // key of score i, 0 for "not a candidate" (0 is the key of a NaN pattern,
+  // which is never a candidate)
+  auto key_of = [&](int i) __attribute__((always_inline)) -> uint32_t {
+    const float s = a.scores[i];
+    return (!isnan(s) && s >= a.min_score) ? order_key(s) : 0u;
+  };
+  // the first NR * kTopkThreads keys stay in registers; the rest are re-read
+  uint32_t kr[NR];
+#pragma unroll
+  for (int j = 0; j < NR; ++j) {
+    const int i = tid + j * kTopkThreads;
+    kr[j] = i < a.N ? key_of(i) : 0u;
+  }
+  auto for_each_key = [&](auto&& fn) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < NR; ++j) fn(kr[j]);
+    for (int i = tid + NR * kTopkThreads; i < a.N; i += kTopkThreads) fn(key_of(i));
+  };
 
-  // candidates
   int cnt = 0;
-  for (int i = tid; i < a.N; i += kTopkThreads) cnt += is_cand(a.scores[i]) ? 1 : 0;
+  for_each_key([&](uint32_t k) __attribute__((always_inline)) { cnt += k != 0u; });
   int n_cand;
   block_scan(cnt, scan_buf, &n_cand);
   const bool take_all = n_cand <= a.k;
@@ -148,40 +167,49 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
   int remaining = a.k;
   if (!take_all) {
     for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int b = tid; b < 256; b += kTopkThreads) hist[b] = 0;
+      if (tid < 256) hist[tid] = 0;
       __syncthreads();
-      for (int i = tid; i < a.N; i += kTopkThreads) {
-        const float s = a.scores[i];
-        if (!is_cand(s)) continue;
-        const uint32_t key = order_key(s);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
-      }
+      for_each_key([&](uint32_t k) __attribute__((always_inline)) {
+        if (k != 0u && (k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
+      });
       __syncthreads();
-      if (tid == 0) {
-        int cum = 0, b = 255;
-        for (; b > 0; --b) {
-          if (cum + hist[b] >= remaining) break;
-          cum += hist[b];
+      if (wave == 0) {
+        // lane l holds bins 255-4l .. 252-4l; find the bin where the count of
+        // keys from the top first reaches `remaining`
+        int c[4], tot = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) { c[e] = hist[255 - 4 * lane - e]; tot += c[e]; }
+        int incl = tot;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o, 64);
+          if (lane >= o) incl += y;
         }
-        sh_bin = b;
-        sh_remaining = remaining - cum;
+        int cum = incl - tot;
+        if (cum < remaining && incl >= remaining) {
+          int e_hit = 3, cum_hit = cum;
+          bool found = false;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (!found && cum + c[e] >= remaining) { found = true; e_hit = e; cum_hit = cum; }
+            cum += c[e];
+          }
+          sh_bin = 255 - 4 * lane - e_hit;
+          sh_remaining = remaining - cum_hit;
+        }
       }
       __syncthreads();
       prefix |= (uint32_t)sh_bin << shift;
       mask |= 255u << shift;
       remaining = sh_remaining;
-      __syncthreads();
     }
   }
   // prefix = key of the k-th best; keys above it are all taken, and
   // `remaining` of those equal to it, earliest first
 
   int taken = 0, eq_seen = 0;
-  for (int i0 = 0; i0 < a.N; i0 += kTopkThreads) {
-    const int i = i0 + tid;
-    const float s = i < a.N ? a.scores[i] : 0.f;
-    const bool cand = i < a.N && is_cand(s);
-    const uint32_t key = cand ? order_key(s) : 0u;
+  auto emit = [&](int i, uint32_t key) __attribute__((always_inline)) {
+    const bool cand = key != 0u;
     const bool gt = cand && (take_all || key > prefix);
     const bool eq = cand && !take_all && key == prefix;
     int eq_tot;
@@ -191,7 +219,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
     const int pos = taken + block_scan(sel ? 1 : 0, scan_buf, &sel_tot);
     if (sel) {
       a.out_chunks[pos] = i;
-      a.out_scores[pos] = s;
+      a.out_scores[pos] = a.scores[i];
       if (a.seg_start) {
         a.seg_start[pos] = a.chunk_start[i];
         a.seg_len[pos] = a.chunk_len[i];
@@ -199,6 +227,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
     }
     taken += sel_tot;
     eq_seen += eq_tot;
+  };
+  // in index order, one block-wide step of kTopkThreads scores at a time
+#pragma unroll
+  for (int j = 0; j < NR; ++j)
+    if (j * kTopkThreads < a.N) emit(tid + j * kTopkThreads, kr[j]);
+  for (int i0 = NR * kTopkThreads; i0 < a.N; i0 += kTopkThreads) {
+    const int i = i0 + tid;
+    emit(i, i < a.N ? key_of(i) : 0u);
   }
   for (int j = taken + tid; j < a.k; j += kTopkThreads) {
     a.out_chunks[j] = -1;

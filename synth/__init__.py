@@ -237,14 +237,17 @@ def _family_sigmas(family: str, d: int):
     raise ValueError(f"unknown input family {family!r}")
 
 
-def make_query_inputs(shape: QueryShape, seed=0, family: str = "F1", num_topics: int = 16) -> QueryInputs:
+def make_query_inputs(shape: QueryShape, seed=0, family: str = "F1", num_topics: int = 16,
+                      query_seed: int = 0) -> QueryInputs:
     """Draw a query-side workload.
 
     Features follow a topic mixture so that similarities spread out: topic
     vectors t_j ~ N(0,1); chunk i gets a topic and feature t + 0.75 N(0,1);
     the query tokens are t_q + N(0,1) for one topic t_q.  Streams:
     PCG64([seed, 1]) lengths and features, PCG64([seed, 2]) query tokens,
-    q and tail, PCG64([seed, 3, i]) chunk i's K/V, PCG64([seed, 4]) sink."""
+    q and tail (PCG64([seed, 2, query_seed]) for query_seed > 0: another
+    query over the same store), PCG64([seed, 3, i]) chunk i's K/V,
+    PCG64([seed, 4]) sink."""
     sh = shape
     sq, sk, sv = _family_sigmas(family, sh.head_dim)
     rng = np.random.Generator(np.random.PCG64([seed, 1]))
@@ -254,7 +257,7 @@ def make_query_inputs(shape: QueryShape, seed=0, family: str = "F1", num_topics:
     which = rng.integers(0, num_topics, sh.num_chunks)
     feat = (topics[which] + np.float32(0.75) * rng.standard_normal((sh.num_chunks, sh.feat_dim),
                                                                    dtype=np.float32)).astype(np.float32)
-    rq = np.random.Generator(np.random.PCG64([seed, 2]))
+    rq = np.random.Generator(np.random.PCG64([seed, 2] if query_seed == 0 else [seed, 2, query_seed]))
     qt = int(rq.integers(0, num_topics))
     query_x = f32_to_bf16_bits(topics[qt][None, :] + rq.standard_normal((sh.q_len, sh.feat_dim), dtype=np.float32))
     q = _draw(rq, (sh.q_len, sh.num_q_heads, sh.head_dim), sq)
