@@ -31,6 +31,7 @@ from .attention import (
     chunk_prefill_attention_rowloop,
     visible_window,
     kv_head_of,
+    acn_window,
 )
 from .ring import RingModel
 from .merge import lse_merge
@@ -43,6 +44,7 @@ __all__ = [
     "chunk_prefill_attention_rowloop",
     "visible_window",
     "kv_head_of",
+    "acn_window",
     "RingModel",
     "lse_merge",
     "token_mean",

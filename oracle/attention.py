@@ -91,13 +91,16 @@ def _check_shapes(q, k_chunk, v_chunk, sink_k, sink_v, hist_k, hist_v, hist_len,
 
 def chunk_prefill_attention(q, k_chunk, v_chunk, sink_k, sink_v, hist_k, hist_v,
                             hist_len: int, window: int, scale: float | None = None,
-                            rows=None, heads=None, block_rows: int = 256):
+                            rows=None, heads=None, block_rows: int = 256, bidirectional: bool = False):
     """Bounded chunk-prefill attention, blocked dense form.
 
     q [C, Hq, d]; k_chunk, v_chunk [C, Hkv, d]; sink_k, sink_v [S, Hkv, d];
     hist_k, hist_v [n, Hkv, d]: the last n >= Wv history tokens in linear
     order (position hist_len - n first).  All float64.
     rows / heads select which chunk rows and query heads to compute.
+    bidirectional: every row sees the whole chunk (Eq. (4) read literally:
+    a vision token sees every token of the chunks in its window, its own
+    chunk included) instead of chunk keys 0..i.
     Returns out [len(rows), len(heads), d] and lse [len(heads), len(rows)].
     """
     C, Hq, Hkv, d, wv = _check_shapes(q, k_chunk, v_chunk, sink_k, sink_v, hist_k, hist_v,
@@ -117,7 +120,8 @@ def chunk_prefill_attention(q, k_chunk, v_chunk, sink_k, sink_v, hist_k, hist_v,
         for b0 in range(0, len(rows), block_rows):
             rb = rows[b0:b0 + block_rows]
             visible = np.ones((len(rb), S + wv + C), dtype=bool)
-            visible[:, S + wv:] = chunk_causal_mask(rb, C)
+            if not bidirectional:
+                visible[:, S + wv:] = chunk_causal_mask(rb, C)
             o, ls = softmax_attention(q[rb, h], keys, vals, visible, scale)
             out[b0:b0 + len(rb), hi] = o
             lse[hi, b0:b0 + len(rb)] = ls
@@ -162,3 +166,17 @@ def chunk_prefill_attention_rowloop(q, k_chunk, v_chunk, sink_k, sink_v, hist_k,
                 out[i, h, c] = math.fsum(ww * float(vv[c]) for ww, vv in zip(w, vs)) / l
             lse[h, i] = m + math.log(l)
     return out, lse
+
+
+def acn_window(chunk_starts, t: int, acn: int) -> int:
+    """History tokens visible to chunk t under the chunk-granular window.
+
+    The vision rows of Eq. (4) see the chunks t-acn .. t (the staircase band);
+    with chunk t starting at linear position chunk_starts[t] (history tokens
+    appended before it), the visible history is chunks max(0, t-acn) .. t-1:
+    chunk_starts[t] - chunk_starts[max(0, t - acn)] tokens.  acn < 0 means the
+    whole history.  The window then goes to chunk_prefill_attention."""
+    starts = np.asarray(chunk_starts, dtype=np.int64)
+    if acn < 0:
+        return int(starts[t])
+    return int(starts[t] - starts[max(0, t - acn)])

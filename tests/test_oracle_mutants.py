@@ -139,3 +139,42 @@ def _merge_pin_holds(attn_mod, merge_mod) -> bool:
 def test_merge_mutants(mut):
     holds = _merge_pin_holds(_load("attention.py"), _load("merge.py", mut))
     assert holds == (mut is None)
+
+
+# ---------------------------------------------------------------- chunk-granular window, bidirectional option
+
+def _acn_pins_hold(mod) -> bool:
+    from tests.test_oracle_acn_pins import _eq4_reference, _stream
+    try:
+        for acn, causal in ((2, False), (1, True), (3, False)):
+            lens, chunks, sk, sv = _stream(7, 4, 2, 16, 3, seed=acn + 30)
+            ref_o, _ = _eq4_reference(lens, chunks, sk, sv, acn, causal)
+            starts = np.concatenate([[0], np.cumsum(lens)])
+            hk = np.concatenate([c[1] for c in chunks])
+            hv = np.concatenate([c[2] for c in chunks])
+            for t, c in enumerate(lens):
+                H = int(starts[t])
+                q, kc, vc = chunks[t]
+                o, _ = mod.chunk_prefill_attention(q, kc, vc, sk, sv, hk[:H], hv[:H], H,
+                                                   mod.acn_window(starts, t, acn), bidirectional=not causal)
+                if np.max(np.abs(o - ref_o[H:H + c])) > 1e-12:
+                    return False
+    except Exception:
+        return False
+    return True
+
+
+ACN_MUTANTS = {
+    "bidirectional_ignored": ("            if not bidirectional:\n", "            if True:\n"),
+    "acn_one_chunk_too_many": ("starts[t] - starts[max(0, t - acn)]", "starts[t] - starts[max(0, t - acn - 1)]"),
+    "acn_counts_current_chunk": ("starts[t] - starts[max(0, t - acn)]", "starts[t] - starts[max(0, t - acn + 1)]"),
+}
+
+
+def test_unmutated_acn_passes():
+    assert _acn_pins_hold(_load("attention.py"))
+
+
+@pytest.mark.parametrize("name", sorted(ACN_MUTANTS))
+def test_acn_mutant_is_caught(name):
+    assert not _acn_pins_hold(_load("attention.py", ACN_MUTANTS[name]))
