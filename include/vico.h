@@ -55,6 +55,8 @@ enum { VICO_DTYPE_BF16 = 0, VICO_DTYPE_F32 = 1 };
 
 #define VICO_FULL_HISTORY (-1)
 #define VICO_SPLIT_BALANCED (-1)
+/* flags of the _ex entry points */
+#define VICO_ATTN_BIDIRECTIONAL 1  /* every chunk row sees the whole chunk (no causal mask) */
 
 /*
  * vico_kv_append -- append a chunk's K/V to the ring-buffer visual cache.
@@ -123,6 +125,40 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
                             int32_t num_splits, void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
+ * vico_chunk_prefill_attn_ex -- vico_chunk_prefill_attn with options.
+ *
+ * flags = 0 is vico_chunk_prefill_attn.  VICO_ATTN_BIDIRECTIONAL: the
+ * additive mask of Eq. (4) read literally -- a vision token sees every token
+ * of the chunks in its window, its own chunk included -- so row i sees
+ * chunk[0 .. chunk_len) instead of chunk[0 .. i].  Other bits are invalid.
+ * Use vico_attn_plan_ex with the same flags for the workspace size.
+ *
+ * The paper's window is whole chunks (the most recent acn chunks, the
+ * staircase band of Eq. (4)); pass window = vico_acn_window(...) to get it
+ * exactly from the caller's table of chunk start positions.
+ */
+int vico_chunk_prefill_attn_ex(const void* q, const void* k_chunk, const void* v_chunk, int32_t chunk_len,
+                               const void* sink_k, const void* sink_v, int32_t sink_len,
+                               const void* ring_k, const void* ring_v, int32_t ring_slots, int64_t hist_len,
+                               int64_t window, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                               float softmax_scale, void* out, int32_t out_dtype, float* lse_out,
+                               int32_t num_splits, int32_t flags, void* workspace, int64_t workspace_bytes,
+                               void* stream);
+
+/*
+ * vico_acn_window -- visible history of chunk t under the chunk-granular
+ * window of Sec. 3 / Eq. (4): the vision rows of chunk t see chunks
+ * t-acn .. t, i.e. the history chunks max(0, t-acn) .. t-1, which is
+ *     chunk_starts[t] - chunk_starts[max(0, t - acn)]
+ * tokens (acn < 0: chunk_starts[t], the whole history).
+ *   chunk_starts  HOST array of num_chunks linear start positions (the number
+ *                 of tokens appended before each chunk), non-decreasing
+ * Returns the window in tokens, or a negative vico_status (t outside the
+ * table, NULL table, decreasing starts).  Host-only arithmetic.
+ */
+int64_t vico_acn_window(const int64_t* chunk_starts, int32_t num_chunks, int32_t t, int32_t acn);
+
+/*
  * vico_attn_plan -- how vico_chunk_prefill_attn will run for these arguments.
  * Host-only; validates the shape arguments exactly as the attention call does.
  *   *num_splits_out      partial results merged per row (1 = no merge)
@@ -132,6 +168,11 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
 int vico_attn_plan(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len,
                    int64_t window, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                    int32_t num_splits, int32_t* num_splits_out, int64_t* workspace_bytes_out);
+
+/* vico_attn_plan for vico_chunk_prefill_attn_ex with the given flags. */
+int vico_attn_plan_ex(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len,
+                      int64_t window, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t num_splits, int32_t flags, int32_t* num_splits_out, int64_t* workspace_bytes_out);
 
 /* Workspace size for vico_chunk_prefill_attn; a negative vico_status on bad arguments. */
 int64_t vico_attn_workspace_bytes(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len,

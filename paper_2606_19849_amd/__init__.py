@@ -15,6 +15,7 @@ from ._binding import (
     VICO_DTYPE_F32,
     VICO_FULL_HISTORY,
     VICO_SPLIT_BALANCED,
+    VICO_ATTN_BIDIRECTIONAL,
     VicoError,
     load_library,
     header_functions,
@@ -27,6 +28,7 @@ from ._binding import (
     vico_topk_chunks,
     vico_gather_plan,
     vico_gather_attn,
+    vico_acn_window,
 )
 
 __all__ = [
@@ -34,6 +36,7 @@ __all__ = [
     "VICO_DTYPE_F32",
     "VICO_FULL_HISTORY",
     "VICO_SPLIT_BALANCED",
+    "VICO_ATTN_BIDIRECTIONAL",
     "VicoError",
     "load_library",
     "header_functions",
@@ -46,4 +49,5 @@ __all__ = [
     "vico_topk_chunks",
     "vico_gather_plan",
     "vico_gather_attn",
+    "vico_acn_window",
 ]

@@ -21,6 +21,7 @@ VICO_DTYPE_BF16 = 0
 VICO_DTYPE_F32 = 1
 VICO_FULL_HISTORY = -1
 VICO_SPLIT_BALANCED = -1
+VICO_ATTN_BIDIRECTIONAL = 1
 
 _i32, _i64, _f32, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
 
@@ -31,6 +32,11 @@ _SIGNATURES = {
     "vico_attn_plan": (_i32, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32,
                               ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "vico_attn_workspace_bytes": (_i64, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32]),
+    "vico_chunk_prefill_attn_ex": (_i32, [_vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _i64, _i64,
+                                          _i32, _i32, _i32, _f32, _vp, _i32, _vp, _i32, _i32, _vp, _i64, _vp]),
+    "vico_attn_plan_ex": (_i32, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
+                                 ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
+    "vico_acn_window": (_i64, [ctypes.POINTER(_i64), _i32, _i32, _i32]),
     "vico_token_mean": (_i32, [_vp, _i32, _i32, _vp, _vp]),
     "vico_chunk_scores": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "vico_topk_chunks": (_i32, [_vp, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -111,14 +117,23 @@ def vico_kv_append(k_chunk, v_chunk, ring_k, ring_v, hist_len: int, stream=None)
 
 
 def vico_attn_plan(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads, head_dim,
-                   num_splits=0):
-    """(splits, workspace_bytes) the attention call will use (vico_attn_plan)."""
+                   num_splits=0, flags: int = 0):
+    """(splits, workspace_bytes) the attention call will use (vico_attn_plan_ex)."""
     ns, wb = _i32(0), _i64(0)
-    st = load_library().vico_attn_plan(chunk_len, sink_len, ring_slots, int(hist_len), int(window),
-                                       num_q_heads, num_kv_heads, head_dim, num_splits,
-                                       ctypes.byref(ns), ctypes.byref(wb))
-    _check(st, "vico_attn_plan")
+    st = load_library().vico_attn_plan_ex(chunk_len, sink_len, ring_slots, int(hist_len), int(window),
+                                          num_q_heads, num_kv_heads, head_dim, num_splits, int(flags),
+                                          ctypes.byref(ns), ctypes.byref(wb))
+    _check(st, "vico_attn_plan_ex")
     return ns.value, wb.value
+
+
+def vico_acn_window(chunk_starts, t: int, acn: int) -> int:
+    """Visible history tokens of chunk t under the acn-chunk window (vico_acn_window)."""
+    arr = (_i64 * len(chunk_starts))(*[int(x) for x in chunk_starts])
+    w = load_library().vico_acn_window(arr, len(chunk_starts), int(t), int(acn))
+    if w < 0:
+        raise VicoError(int(w), "vico_acn_window")
+    return w
 
 
 def vico_attn_workspace_bytes(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads,
@@ -132,8 +147,8 @@ def vico_attn_workspace_bytes(chunk_len, sink_len, ring_slots, hist_len, window,
 
 def vico_chunk_prefill_attn(q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v, hist_len: int, window: int,
                             out, lse=None, workspace=None, num_splits: int = 0, softmax_scale: float = 0.0,
-                            stream=None) -> None:
-    """Bounded chunk-prefill attention (vico_chunk_prefill_attn); writes `out` (and `lse`)."""
+                            stream=None, flags: int = 0) -> None:
+    """Bounded chunk-prefill attention (vico_chunk_prefill_attn_ex); writes `out` (and `lse`)."""
     for n, t in (("q", q), ("k_chunk", k_chunk), ("v_chunk", v_chunk), ("sink_k", sink_k),
                  ("sink_v", sink_v), ("ring_k", ring_k), ("ring_v", ring_v)):
         _dev_bf16(n, t)
@@ -150,11 +165,11 @@ def vico_chunk_prefill_attn(q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v,
         raise ValueError("lse: expected a contiguous float32 CUDA tensor of shape [num_q_heads, chunk_len]")
     wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
     odt = VICO_DTYPE_F32 if out.dtype == torch.float32 else VICO_DTYPE_BF16
-    st = load_library().vico_chunk_prefill_attn(
+    st = load_library().vico_chunk_prefill_attn_ex(
         _ptr(q), _ptr(k_chunk), _ptr(v_chunk), C, _ptr(sink_k), _ptr(sink_v), S, _ptr(ring_k), _ptr(ring_v), R,
         int(hist_len), int(window), Hq, Hkv, D, float(softmax_scale), _ptr(out), odt, _ptr(lse),
-        int(num_splits), _ptr(workspace), wb, _stream(stream))
-    _check(st, "vico_chunk_prefill_attn")
+        int(num_splits), int(flags), _ptr(workspace), wb, _stream(stream))
+    _check(st, "vico_chunk_prefill_attn_ex")
 
 
 def _dev_tensor(name, t, dtype, ndim):

@@ -39,7 +39,9 @@
 //     past the chunk end read as zero the same way.  No copies are made.
 //   * Causal chunk: only tiles that reach past the first row of a wave run the
 //     masked variant of the tile body; tiles beyond the last row of a wave are
-//     skipped by that wave.
+//     skipped by that wave.  With the bidirectional option (Eq. (4) read
+//     literally: a chunk sees all of itself) every row's last key is the
+//     chunk's last key, so only the tile holding the chunk end is masked.
 //   * Work-groups are renumbered so that consecutive logical ids (the query
 //     heads of one KV head) land on the same XCD and share its L2.
 //   * Optional split of the key range (for chunks too small to fill 256 CUs):
@@ -104,9 +106,14 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   const int hh = lane >> 5;
 
   const int C = a.C, S = a.S, SW = a.S + a.Wv;
-  // key tiles seen by row tile rt: keys up to the last row's own position
+  // last key visible to chunk row `row`: its own position (causal), or the
+  // chunk's last key when the chunk attends to itself bidirectionally
+  auto last_key_of_row = [&](int row) __attribute__((always_inline)) {
+    return SW + (a.bidir ? C - 1 : min(row, C - 1));
+  };
+  // key tiles seen by row tile rt: keys up to its last row's last key
   auto tiles_of = [&](int rt) __attribute__((always_inline)) {
-    return (SW + min((rt + 1) * BM, C) + BN - 1) / BN;
+    return (last_key_of_row((rt + 1) * BM - 1) + BN) / BN;
   };
 
   // ---- one segment of work: key tiles [t_lo, t_hi) of row tile rt of query
@@ -122,11 +129,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   // this wave: rows wrow0 + rb*32 + l32, rb < RB
   const int wrow0 = row0 + wave * 32 * RB;
   const bool wave_active = wrow0 < C;
-  const int wave_first_lim = SW + min(wrow0, C - 1);            // last key of the wave's first row
-  const int wave_last_lim = SW + min(wrow0 + 32 * RB - 1, C - 1);
+  const int wave_first_lim = last_key_of_row(wrow0);              // last key of the wave's first row
+  const int wave_last_lim = last_key_of_row(wrow0 + 32 * RB - 1);
   int key_lim[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) key_lim[rb] = SW + min(wrow0 + rb * 32 + l32, C - 1);
+  for (int rb = 0; rb < RB; ++rb) key_lim[rb] = last_key_of_row(wrow0 + rb * 32 + l32);
 
   // ---- Q rows of this wave as MFMA B fragments (lane: row l32, dims hh*8..+8)
   bf16x8 qf[RB][NKS];

@@ -27,15 +27,17 @@ bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
 }
 
 struct Shape {
-  int C, S, R, Wv, ws, Hq, Hkv, D, splits, balanced, grid;
+  int C, S, R, Wv, ws, Hq, Hkv, D, splits, balanced, grid, bidir;
   int64_t total_tiles;
   int64_t ws_bytes;
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
-int64_t tiles_of(int rt, int C, int SW) {
-  const int64_t last = std::min<int64_t>(int64_t(rt + 1) * vico::kBlockM, C);
+// Key tiles of row tile rt: up to its last row's last visible key (the
+// kernel's rule: the row's own position, or the chunk end when bidirectional).
+int64_t tiles_of(int rt, int C, int SW, int bidir) {
+  const int64_t last = bidir ? C : std::min<int64_t>(int64_t(rt + 1) * vico::kBlockM, C);
   return (SW + last + vico::kKeyTile - 1) / vico::kKeyTile;
 }
 
@@ -56,11 +58,11 @@ int plan_splits(int C, int S, int Wv, int Hq, int request) {
 // Balanced plan: gridDim.x equal shares of the (row tile, key tile) pairs.
 // Returns the largest number of work-groups any row tile is spread over, or
 // 0 when the balanced schedule does not apply.
-int plan_balanced(int C, int SW, int Hq, int Hkv, int64_t* total, int* grid) {
+int plan_balanced(int C, int SW, int Hq, int Hkv, int bidir, int64_t* total, int* grid) {
   const int n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
   const int g = Hq / Hkv;
   int64_t T = 0;
-  for (int rt = 0; rt < n_rt; ++rt) T += int64_t(Hq) * tiles_of(rt, C, SW);
+  for (int rt = 0; rt < n_rt; ++rt) T += int64_t(Hq) * tiles_of(rt, C, SW, bidir);
   const int64_t G = int64_t(vico::kNumCUs) * vico::kWgPerCU;
   if (T < 4 * G) return 0;
   // walk the row tiles in kernel order: kv, row tile (longest first), query head
@@ -68,7 +70,7 @@ int plan_balanced(int C, int SW, int Hq, int Hkv, int64_t* total, int* grid) {
   int64_t start = 0;
   for (int kv = 0; kv < Hkv; ++kv)
     for (int ri = 0; ri < n_rt; ++ri) {
-      const int64_t n = tiles_of(n_rt - 1 - ri, C, SW);
+      const int64_t n = tiles_of(n_rt - 1 - ri, C, SW, bidir);
       for (int qh = 0; qh < g; ++qh) {
         const int64_t w0 = ((start + 1) * G - 1) / T, w1 = ((start + n) * G - 1) / T;
         max_parts = (int)std::max<int64_t>(max_parts, w1 - w0 + 1);
@@ -83,8 +85,10 @@ int plan_balanced(int C, int SW, int Hq, int Hkv, int64_t* total, int* grid) {
 
 // Validates everything the attention call and the planner share.
 int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int32_t Hq, int32_t Hkv,
-                     int32_t D, int32_t splits, Shape* sh) {
+                     int32_t D, int32_t splits, int32_t flags, Shape* sh) {
   if (C < 0 || S < 0 || R < 0 || H < 0 || W < -1 || splits < VICO_SPLIT_BALANCED) return VICO_ERR_INVALID_ARG;
+  if (flags & ~VICO_ATTN_BIDIRECTIONAL) return VICO_ERR_INVALID_ARG;
+  const int bidir = (flags & VICO_ATTN_BIDIRECTIONAL) ? 1 : 0;
   if (Hq < 1 || Hkv < 1 || Hq > kMaxHeads || Hq % Hkv != 0) return VICO_ERR_INVALID_ARG;
   if (D != 64 && D != 128) return VICO_ERR_UNSUPPORTED;
   if (C > kMaxChunk || S > kMaxChunk) return VICO_ERR_INVALID_ARG;
@@ -98,6 +102,7 @@ int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int3
   sh->C = C; sh->S = S; sh->R = R; sh->Wv = (int)wv;
   sh->ws = R > 0 ? (int)((H - wv) % R) : 0;
   sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;
+  sh->bidir = bidir;
   sh->splits = 1;
   sh->balanced = 0;
   sh->total_tiles = 0;
@@ -111,7 +116,7 @@ int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int3
     // balance gains -- the chip runs power-limited and idle CUs raise the clock)
     if (splits == VICO_SPLIT_BALANCED ||
         (splits == 0 && 2 * int64_t(Hq) * n_rt * ns <= int64_t(vico::kNumCUs) * vico::kWgPerCU))
-      parts = plan_balanced(C, S + (int)wv, Hq, Hkv, &sh->total_tiles, &sh->grid);
+      parts = plan_balanced(C, S + (int)wv, Hq, Hkv, bidir, &sh->total_tiles, &sh->grid);
     if (parts > 0) {
       sh->balanced = 1;
       sh->splits = parts;
@@ -194,9 +199,16 @@ int vico_last_hip_error(void) { return g_last_hip_error; }
 int vico_attn_plan(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len, int64_t window,
                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t num_splits,
                    int32_t* num_splits_out, int64_t* workspace_bytes_out) {
+  return vico_attn_plan_ex(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads, head_dim,
+                           num_splits, 0, num_splits_out, workspace_bytes_out);
+}
+
+int vico_attn_plan_ex(int32_t chunk_len, int32_t sink_len, int32_t ring_slots, int64_t hist_len, int64_t window,
+                      int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t num_splits, int32_t flags,
+                      int32_t* num_splits_out, int64_t* workspace_bytes_out) {
   Shape sh;
   const int st = check_attn_shape(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads,
-                                  head_dim, num_splits, &sh);
+                                  head_dim, num_splits, flags, &sh);
   if (st != VICO_OK) return st;
   if (num_splits_out) *num_splits_out = sh.splits;
   if (workspace_bytes_out) *workspace_bytes_out = sh.ws_bytes;
@@ -218,9 +230,20 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
                             int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float softmax_scale,
                             void* out, int32_t out_dtype, float* lse_out, int32_t num_splits, void* workspace,
                             int64_t workspace_bytes, void* stream) {
+  return vico_chunk_prefill_attn_ex(q, k_chunk, v_chunk, chunk_len, sink_k, sink_v, sink_len, ring_k, ring_v,
+                                    ring_slots, hist_len, window, num_q_heads, num_kv_heads, head_dim, softmax_scale,
+                                    out, out_dtype, lse_out, num_splits, 0, workspace, workspace_bytes, stream);
+}
+
+int vico_chunk_prefill_attn_ex(const void* q, const void* k_chunk, const void* v_chunk, int32_t chunk_len,
+                               const void* sink_k, const void* sink_v, int32_t sink_len, const void* ring_k,
+                               const void* ring_v, int32_t ring_slots, int64_t hist_len, int64_t window,
+                               int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float softmax_scale,
+                               void* out, int32_t out_dtype, float* lse_out, int32_t num_splits, int32_t flags,
+                               void* workspace, int64_t workspace_bytes, void* stream) {
   Shape sh;
   int st = check_attn_shape(chunk_len, sink_len, ring_slots, hist_len, window, num_q_heads, num_kv_heads, head_dim,
-                            num_splits, &sh);
+                            num_splits, flags, &sh);
   if (st != VICO_OK) return st;
   if (out_dtype != VICO_DTYPE_BF16 && out_dtype != VICO_DTYPE_F32) return VICO_ERR_UNSUPPORTED;
   if (isnan(softmax_scale) || isinf(softmax_scale)) return VICO_ERR_INVALID_ARG;
@@ -268,10 +291,19 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
   a.balanced = sh.balanced;
   a.total_tiles = sh.total_tiles;
   a.out_f32 = out_dtype == VICO_DTYPE_F32;
+  a.bidir = sh.bidir;
   const double scale = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(head_dim));
   a.scale_log2 = (float)(scale * 1.4426950408889634);
   const hipError_t e = vico::launch_attention(a, sh.grid, (hipStream_t)stream);
   return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
+int64_t vico_acn_window(const int64_t* chunk_starts, int32_t num_chunks, int32_t t, int32_t acn) {
+  if (!chunk_starts || num_chunks < 1 || t < 0 || t >= num_chunks) return VICO_ERR_INVALID_ARG;
+  if (acn < 0) return chunk_starts[t];
+  const int32_t first = t - acn > 0 ? t - acn : 0;
+  const int64_t w = chunk_starts[t] - chunk_starts[first];
+  return w < 0 ? int64_t(VICO_ERR_INVALID_ARG) : w;
 }
 
 int vico_kv_append(const void* k_chunk, const void* v_chunk, int32_t chunk_len, void* ring_k, void* ring_v,

@@ -41,6 +41,7 @@ struct AttnArgs {
   int balanced;        // 1: work-groups take equal shares of all key tiles
   int64_t total_tiles; // balanced mode: key tiles summed over all row tiles and heads
   int out_f32;
+  int bidir;           // 1: every chunk row sees the whole chunk (no causal mask)
   float scale_log2;    // softmax scale * log2(e)
 };
 

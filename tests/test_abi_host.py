@@ -15,7 +15,8 @@ MIS = 0x10008
 
 EXPECTED = {"vico_kv_append", "vico_chunk_prefill_attn", "vico_attn_plan", "vico_attn_workspace_bytes",
             "vico_status_str", "vico_last_hip_error", "vico_token_mean", "vico_chunk_scores", "vico_topk_chunks",
-            "vico_gather_plan", "vico_gather_attn"}
+            "vico_gather_plan", "vico_gather_attn", "vico_chunk_prefill_attn_ex", "vico_attn_plan_ex",
+            "vico_acn_window"}
 
 
 def test_header_declares_the_expected_entry_points():
@@ -262,3 +263,44 @@ def test_gather_plan_parts():
     p, wb = vico.vico_gather_plan(1, 1, 0, 256, 2, 256, 2, 1, 64, num_splits=3)
     assert p == 3 and wb == 256 * ((3 * 2 * 1 * 64 * 4 + 255) // 256) + 3 * 2 * 4
     assert vico.vico_gather_plan(1, 1, 0, 256, 2, 256, 2, 1, 64, num_splits=500)[0] == 64
+
+
+# ---------------------------------------------------------------- options and the chunk-granular window
+
+def test_unknown_attention_flags_are_rejected():
+    st = lib.vico_chunk_prefill_attn_ex(A, A + 0x100000, A + 0x200000, 64, A + 0x300000, A + 0x400000, 16,
+                                        A + 0x500000, A + 0x600000, 256, 456, 256, 2, 1, 64, 0.0, B, 1, None, 0, 2,
+                                        None, 0, None)
+    assert st == -1
+    assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, 0, 1) == vico.vico_attn_plan(64, 16, 256, 456,
+                                                                                              256, 2, 1, 64, 0, 0)
+    with pytest.raises(vico.VicoError):
+        vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, 0, 4)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_acn_window_matches_oracle(seed):
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(seed)
+    starts = np.concatenate([[0], np.cumsum(rng.integers(0, 900, 40))])
+    for t in range(len(starts)):
+        for acn in (-1, 0, 1, 2, 4, 8, 100):
+            assert vico.vico_acn_window(list(starts), t, acn) == oracle.acn_window(starts, t, acn)
+
+
+def test_acn_window_rejects_bad_tables():
+    arr = (ctypes.c_int64 * 3)(0, 10, 5)
+    assert lib.vico_acn_window(arr, 3, 3, 1) == -1          # t outside the table
+    assert lib.vico_acn_window(arr, 3, -1, 1) == -1
+    assert lib.vico_acn_window(None, 3, 1, 1) == -1
+    assert lib.vico_acn_window(arr, 3, 2, 1) == -1          # decreasing starts
+
+
+def test_balanced_plan_counts_whole_chunks_when_bidirectional():
+    # bidirectional rows all see the whole chunk: more key tiles, possibly more parts
+    c = dict(chunk_len=600, sink_len=64, ring_slots=4596, hist_len=4596, window=4000, num_q_heads=8,
+             num_kv_heads=2, head_dim=128, num_splits=vico.VICO_SPLIT_BALANCED)
+    causal = vico.vico_attn_plan(**c)
+    bidir = vico.vico_attn_plan(**c, flags=vico.VICO_ATTN_BIDIRECTIONAL)
+    assert bidir[0] >= causal[0] >= 1

@@ -1,0 +1,75 @@
+"""GPU parity of the bidirectional in-chunk option and of the chunk-granular
+acn window (paper, Sec. 3 and the staircase mask of Eq. (4)) against the
+oracle, whose readings are pinned to the literal mask in
+test_oracle_acn_pins.py.  Tolerances as in test_gpu_parity.py."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_19849_amd as vico
+from synth import make_chunk_inputs, ragged_chunk_lengths, stream_chunk, stream_sink
+from tests._gpu import DeviceChunk, check_bf16, check_f32, dev, oracle_result
+from tests.test_gpu_parity import SMALL
+
+pytestmark = pytest.mark.gpu
+BIDIR = vico.VICO_ATTN_BIDIRECTIONAL
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+@pytest.mark.parametrize("splits", [0, 1, 3, -1])
+def test_bidirectional_small_f2_fp32(name, splits):
+    inp = make_chunk_inputs(SMALL[name], seed=301, family="F2")
+    o, lse = DeviceChunk(inp).attention(torch.float32, num_splits=splits, flags=BIDIR)
+    ref, ref_lse = oracle_result(inp, bidirectional=True)
+    check_f32(o, ref, lse, ref_lse)
+
+
+@pytest.mark.parametrize("name", ["tiny", "gqa7_ragged", "balanced_many_parts"])
+def test_bidirectional_bf16(name):
+    inp = make_chunk_inputs(SMALL[name], seed=302, family="F2")
+    o, _ = DeviceChunk(inp).attention(torch.bfloat16, flags=BIDIR)
+    check_bf16(o, oracle_result(inp, bidirectional=True)[0])
+
+
+@pytest.mark.parametrize("flags", [0, BIDIR])
+def test_acn_window_stream(flags):
+    """32 ragged chunks (256..1024 tokens) at 3B heads with the window set to
+    the 4 most recent whole chunks; the ring holds 4 * 1024 slots, so the
+    window read wraps; attend then append per chunk."""
+    Hq, Hkv, D, S, acn, R = 16, 2, 128, 64, 4, 4096
+    counts = ragged_chunk_lengths(32, 256, 1024, seed=3)
+    starts = np.concatenate([[0], np.cumsum(counts)])
+    sk_bits, sv_bits = stream_sink(S, Hkv, D, seed=3, family="F2")
+    sk, sv = dev(sk_bits), dev(sv_bits)
+    rk = torch.zeros((R, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    rv = torch.zeros_like(rk)
+    sk64, sv64 = oracle.bf16_bits_to_f64(sk_bits), oracle.bf16_bits_to_f64(sv_bits)
+    hk_all, hv_all = [], []
+    rng = np.random.default_rng(7)
+    ws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    for t, c in enumerate(counts):
+        c = int(c)
+        H = int(starts[t])
+        W = vico.vico_acn_window(list(starts[:t + 1]), t, acn)
+        assert W == oracle.acn_window(starts, t, acn)
+        qb, kb, vb = stream_chunk(t, c, Hq, Hkv, D, seed=3, family="F2")
+        q, k, v = dev(qb), dev(kb), dev(vb)
+        out = torch.empty((c, Hq, D), dtype=torch.float32, device="cuda")
+        lse = torch.empty((Hq, c), dtype=torch.float32, device="cuda")
+        assert vico.vico_attn_plan(c, S, R, H, W, Hq, Hkv, D, 0, flags)[1] <= ws.numel()
+        vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, H, W, out, lse=lse, workspace=ws, flags=flags)
+        vico.vico_kv_append(k, v, rk, rv, H)
+        rows = np.unique(np.concatenate([[0, c - 1], rng.choice(c, 8, replace=False)]))
+        o = out[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+        l = lse[:, torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+        hk = np.concatenate(hk_all) if hk_all else np.zeros((0, Hkv, D))
+        hv = np.concatenate(hv_all) if hv_all else np.zeros((0, Hkv, D))
+        ref, ref_lse = oracle.chunk_prefill_attention(
+            oracle.bf16_bits_to_f64(qb), oracle.bf16_bits_to_f64(kb), oracle.bf16_bits_to_f64(vb),
+            sk64, sv64, hk, hv, H, W, rows=rows, bidirectional=bool(flags & BIDIR))
+        check_f32(o, ref, l, ref_lse)
+        hk_all.append(oracle.bf16_bits_to_f64(kb))
+        hv_all.append(oracle.bf16_bits_to_f64(vb))
+        if len(hk_all) > acn + 1:
+            hk_all, hv_all = hk_all[1:], hv_all[1:]
