@@ -19,9 +19,12 @@ Modules
   merge      -- log-sum-exp merge of attention over disjoint key sets
   retrieval  -- query-side chunk retrieval (token means, cosine scores,
                 top-k selection) and attention over the retrieved chunks
+  token_drop -- chunk-level temporal token dropping (pairwise cosine over
+                frames, anchor frame) and the retained-token order
 
 Parity status: every function here is pinned by tests in
-tests/test_oracle_pins.py and tests/test_oracle_retrieval_pins.py against library routines, closed forms,
+tests/test_oracle_pins.py, tests/test_oracle_retrieval_pins.py,
+tests/test_oracle_acn_pins.py and tests/test_oracle_drop_pins.py against library routines, closed forms,
 invariants and brute force; none is "parity unpinned".
 """
 from .bf16 import bf16_bits_to_f64
@@ -36,6 +39,7 @@ from .attention import (
 from .ring import RingModel
 from .merge import lse_merge
 from .retrieval import token_mean, cosine_scores, select_chunks, chunk_segments, gather_attention
+from .token_drop import temporal_drop, gather_tokens, NO_COMPARISON
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -52,4 +56,7 @@ __all__ = [
     "select_chunks",
     "chunk_segments",
     "gather_attention",
+    "temporal_drop",
+    "gather_tokens",
+    "NO_COMPARISON",
 ]

@@ -32,6 +32,8 @@ __all__ = [
     "make_query_inputs",
     "make_tokens",
     "QUERY_CONFIGS",
+    "make_drop_frames",
+    "DROP_CONFIGS",
 ]
 
 
@@ -283,4 +285,50 @@ QUERY_CONFIGS = {
     "q_gqa7": QueryShape(14, 2, 128, 4, 384, 30, 1, 300, 9, 21, 7),
     "q_7b": QueryShape(28, 4, 128, 64, 3584, 256, 256, 1024, 32, 32, 32),
     "q_3b": QueryShape(16, 2, 128, 64, 2048, 256, 256, 1024, 32, 32, 32),
+}
+
+
+# ---------------------------------------------------------------------------
+# Temporal token dropping: projected visual tokens of consecutive frames.
+# ---------------------------------------------------------------------------
+
+def make_drop_frames(num_chunks: int, frames_per_chunk: int, tokens_per_frame: int, feat_dim: int,
+                     static_frac: float = 0.5, noise: float = 0.15, seed: int = 0) -> np.ndarray:
+    """bf16 bits [B, c, n_f, dm] of projected tokens with static and moving regions.
+
+    Every position gets a base vector ~ N(0,1).  A static position (a fraction
+    static_frac, fixed per position for the whole batch) shows the base plus
+    noise * N(0,1) in every frame, so its frames are nearly parallel (cosine
+    about 1 / (1 + noise^2)); a moving position draws a fresh N(0,1) vector
+    per frame (cosine about 0).  A few positions use noise levels spread
+    around the usual thresholds so that similarities fall close to them.
+    Drawn from PCG64([seed, 6])."""
+    rng = np.random.Generator(np.random.PCG64([seed, 6]))
+    B, c, n_f, dm = num_chunks, frames_per_chunk, tokens_per_frame, feat_dim
+    static = rng.random(n_f) < static_frac
+    level = np.full(n_f, noise, dtype=np.float32)
+    near = rng.random(n_f) < 0.1
+    level[near] = rng.uniform(0.2, 0.6, int(near.sum())).astype(np.float32)
+    out = np.empty((B, c, n_f, dm), dtype=np.uint16)
+    base = rng.standard_normal((n_f, dm), dtype=np.float32)
+    for b in range(B):
+        for f in range(c):
+            fresh = rng.standard_normal((n_f, dm), dtype=np.float32)
+            x = np.where(static[:, None], base + level[:, None] * fresh, fresh)
+            out[b, f] = f32_to_bf16_bits(x)
+        if rng.random() < 0.3:                     # the scene changes between chunks now and then
+            base = rng.standard_normal((n_f, dm), dtype=np.float32)
+    return out
+
+
+# (num_chunks, frames per chunk, tokens per frame, feature dim): Qwen2.5-VL
+# merges 2x2 patches of 14 px, so a 448x448 frame gives 16 x 16 = 256 tokens;
+# 4 frames per chunk give the 1024-token chunks of the streaming workload.
+DROP_CONFIGS = {
+    "tiny": (3, 4, 24, 64),
+    "c2": (2, 2, 40, 128),
+    "c1": (6, 1, 32, 96),
+    "c8": (1, 8, 50, 256),
+    "7b": (16, 4, 256, 3584),
+    "3b": (16, 4, 256, 2048),
 }

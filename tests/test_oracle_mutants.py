@@ -178,3 +178,58 @@ def test_unmutated_acn_passes():
 @pytest.mark.parametrize("name", sorted(ACN_MUTANTS))
 def test_acn_mutant_is_caught(name):
     assert not _acn_pins_hold(_load("attention.py", ACN_MUTANTS[name]))
+
+
+# ---------------------------------------------------------------- temporal token dropping
+
+def _drop_pins_hold(mod) -> bool:
+    import itertools
+    from scipy.spatial.distance import cdist
+    import oracle
+    from synth import make_drop_frames
+    from tests.test_oracle_drop_pins import _brute
+    f64 = oracle.bf16_bits_to_f64
+    try:
+        for shape, tau in (((3, 4, 24, 64), 0.9), ((2, 3, 30, 32), 0.0)):
+            z = f64(make_drop_frames(*shape, seed=sum(shape)))
+            keep, _, index = mod.temporal_drop(z, tau)
+            bk, bi = _brute(z, tau)
+            if not (np.array_equal(keep, bk) and np.array_equal(index, bi)):
+                return False
+        z = f64(make_drop_frames(6, 1, 32, 96, seed=3))
+        keep, _, index = mod.temporal_drop(z, 0.7)
+        bk, bi = _brute(z, 0.7)
+        if not (np.array_equal(keep, bk) and np.array_equal(index, bi)):
+            return False
+        z = np.zeros((1, 2, 1, 4))
+        z[0, 0, 0, :2] = (3, 4)
+        z[0, 1, 0, :2] = (4, 3)
+        if not mod.temporal_drop(z, 0.96)[0][0, 0]:
+            return False
+        a, b = np.eye(3)[0], np.eye(3)[1]
+        z = np.stack([a, (a + b) / np.sqrt(2), b])[None, :, None, :]
+        if not mod.temporal_drop(z, 0.5)[0][0, 0]:
+            return False
+    except Exception:
+        return False
+    return True
+
+
+DROP_MUTANTS = {
+    "threshold_not_strict": ("drop &= s_ij > tau", "drop &= s_ij >= tau"),
+    # "any pair exceeds" instead of "all pairs exceed"
+    "any_pair_drops": ("drop &= s_ij > tau", "drop = (drop & (i > 0)) | (s_ij > tau)"),
+    "neighbours_only": ("for j in range(i + 1, c):", "for j in range(i + 1, min(i + 2, c)):"),
+    "anchor_dropped": ("if (c > 1 and f == 0) or keep[b, p]:", "if keep[b, p]:"),
+    "compare_with_next_frame": ("before = z[b - 1, 0] if b > 0 else prev", "before = z[b + 1, 0] if b + 1 < B else prev"),
+    "position_major_order": ("for f in range(c):\n            for p in range(n_f):", "for p in range(n_f):\n            for f in range(c):"),
+}
+
+
+def test_unmutated_drop_passes():
+    assert _drop_pins_hold(_load("token_drop.py"))
+
+
+@pytest.mark.parametrize("name", sorted(DROP_MUTANTS))
+def test_drop_mutant_is_caught(name):
+    assert not _drop_pins_hold(_load("token_drop.py", DROP_MUTANTS[name]))
