@@ -283,6 +283,39 @@ int vico_gather_plan(int32_t q_len, int32_t tail_len, int32_t sink_len, int32_t 
                      int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
                      int32_t head_dim, int32_t num_splits, int32_t* num_splits_out, int64_t* workspace_bytes_out);
 
+/*
+ * vico_temporal_drop -- chunk-level temporal token dropping (Sec. 3, "Token
+ * Dropping", the pairwise-similarity and drop equations).
+ *
+ * For each of num_chunks consecutive chunks of C = frames_per_chunk frames
+ * and each spatial position p, the cosine of the frames' tokens at p is taken
+ * for every frame pair i < j; p is dropped when all of them exceed tau
+ * (strictly), and the chunk's first frame is always kept (the anchor), so a
+ * dropped position keeps only its frame-1 token.  With C = 1 every frame is
+ * compared with the frame before it (prev_frame for the first one; with
+ * prev_frame NULL the first frame is kept whole) and there is no anchor.
+ * Cosines are fp32 sums of the bf16 products; a zero vector scores 0.
+ *
+ *   frames      [num_chunks][C][tokens_per_frame][feat_dim] bf16, device
+ *   prev_frame  [tokens_per_frame][feat_dim] bf16 or NULL (C = 1 only; ignored otherwise)
+ *   keep        [num_chunks][tokens_per_frame] uint8, written: 1 = position kept
+ *   sim         NULL or [num_chunks][tokens_per_frame] fp32, written: the
+ *               smallest pairwise cosine (C = 1: the cosine with the previous
+ *               frame, -2 where there is none); keep == !(sim > tau) exactly
+ *   out_tokens  NULL or capacity for num_chunks*C*tokens_per_frame rows of
+ *               feat_dim bf16: the retained tokens, in stream order (chunk,
+ *               frame, position), bit copies of the inputs
+ *   out_index   [num_chunks*C*tokens_per_frame] int32: flat source row
+ *               (chunk*C + frame)*tokens_per_frame + position of each
+ *               retained token, in the same order
+ *   out_count   [1] int32: number of retained tokens
+ * 1 <= C <= 8, feat_dim a positive multiple of 8, fewer than 2^31 rows;
+ * num_chunks == 0 is a no-op.  Two kernels, no workspace.
+ */
+int vico_temporal_drop(const void* frames, int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
+                       int32_t feat_dim, float tau, const void* prev_frame, uint8_t* keep, float* sim,
+                       void* out_tokens, int32_t* out_index, int32_t* out_count, void* stream);
+
 /* Static text for a vico_status value. */
 const char* vico_status_str(int status);
 

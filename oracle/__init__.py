@@ -39,7 +39,7 @@ from .attention import (
 from .ring import RingModel
 from .merge import lse_merge
 from .retrieval import token_mean, cosine_scores, select_chunks, chunk_segments, gather_attention
-from .token_drop import temporal_drop, gather_tokens, NO_COMPARISON
+from .token_drop import temporal_drop, retained_index, gather_tokens, NO_COMPARISON
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -57,6 +57,7 @@ __all__ = [
     "chunk_segments",
     "gather_attention",
     "temporal_drop",
+    "retained_index",
     "gather_tokens",
     "NO_COMPARISON",
 ]

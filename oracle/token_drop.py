@@ -72,13 +72,22 @@ def temporal_drop(z: np.ndarray, tau: float, prev: np.ndarray | None = None):
                 s = _cos(z[b, 0], np.asarray(before, dtype=np.float64))
                 sim[b] = s
                 keep[b] = ~(s > tau)
+    return keep, sim, retained_index(keep, c)
+
+
+def retained_index(keep: np.ndarray, c: int) -> np.ndarray:
+    """Flat source rows of the retained tokens, in stream order, for the
+    position decisions `keep` [B, n_f] of chunks of c frames: every token of
+    the anchor frame (c > 1), and the tokens of kept positions in the other
+    frames (all frames when c = 1)."""
+    B, n_f = keep.shape
     index = []
     for b in range(B):
         for f in range(c):
             for p in range(n_f):
                 if (c > 1 and f == 0) or keep[b, p]:
                     index.append((b * c + f) * n_f + p)
-    return keep, sim, np.asarray(index, dtype=np.int64)
+    return np.asarray(index, dtype=np.int64)
 
 
 def gather_tokens(z: np.ndarray, index: np.ndarray) -> np.ndarray:

@@ -6,7 +6,8 @@ to a sink prefix, the W newest cached visual tokens and themselves
 (causally) under grouped-query attention; the chunk's K/V then enter a
 ring-buffer cache.  Query-side retrieval (token means, cosine scores, top-k
 chunks) and attention of short queries or decode steps over the retrieved
-chunks complete the query path.  All arithmetic runs in the hand-written HIP
+chunks complete the query path; temporal token dropping thins each chunk's
+tokens before they reach the LLM.  All arithmetic runs in the hand-written HIP
 kernels of libvico.so (C ABI in include/vico.h); this package only marshals
 arguments.
 """
@@ -29,6 +30,7 @@ from ._binding import (
     vico_gather_plan,
     vico_gather_attn,
     vico_acn_window,
+    vico_temporal_drop,
 )
 
 __all__ = [
@@ -50,4 +52,5 @@ __all__ = [
     "vico_gather_plan",
     "vico_gather_attn",
     "vico_acn_window",
+    "vico_temporal_drop",
 ]

@@ -37,6 +37,7 @@ _SIGNATURES = {
     "vico_attn_plan_ex": (_i32, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
                                  ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "vico_acn_window": (_i64, [ctypes.POINTER(_i64), _i32, _i32, _i32]),
+    "vico_temporal_drop": (_i32, [_vp, _i32, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "vico_token_mean": (_i32, [_vp, _i32, _i32, _vp, _vp]),
     "vico_chunk_scores": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "vico_topk_chunks": (_i32, [_vp, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -264,3 +265,29 @@ def vico_gather_attn(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_st
         cap, _ptr(seg_start), _ptr(seg_len), n_segs, int(keys_hint), Hq, Hkv, D, float(softmax_scale), _ptr(out),
         odt, _ptr(lse), int(num_splits), _ptr(workspace), wb, _stream(stream))
     _check(st, "vico_gather_attn")
+
+
+def vico_temporal_drop(frames, tau: float, keep, out_index, out_count, sim=None, out_tokens=None, prev_frame=None,
+                       stream=None) -> None:
+    """Chunk-level temporal token dropping (vico_temporal_drop); frames bf16 [B, C, n_f, dm]."""
+    _dev_tensor("frames", frames, torch.bfloat16, 4)
+    B, C, n_f, dm = frames.shape
+    _dev_tensor("keep", keep, torch.uint8, 2)
+    _dev_tensor("out_index", out_index, torch.int32, 1)
+    _dev_tensor("out_count", out_count, torch.int32, 1)
+    if tuple(keep.shape) != (B, n_f) or out_index.shape[0] < B * C * n_f:
+        raise ValueError("keep must be [B, n_f] and out_index hold B*C*n_f entries")
+    if sim is not None:
+        _dev_tensor("sim", sim, torch.float32, 2)
+        if tuple(sim.shape) != (B, n_f):
+            raise ValueError("sim must be [B, n_f]")
+    if out_tokens is not None:
+        _dev_tensor("out_tokens", out_tokens, torch.bfloat16, 2)
+        if out_tokens.shape[0] < B * C * n_f or out_tokens.shape[1] != dm:
+            raise ValueError("out_tokens must hold B*C*n_f rows of dm")
+    if prev_frame is not None:
+        _dev_tensor("prev_frame", prev_frame, torch.bfloat16, 2)
+    st = load_library().vico_temporal_drop(_ptr(frames), B, C, n_f, dm, float(tau), _ptr(prev_frame), _ptr(keep),
+                                           _ptr(sim), _ptr(out_tokens), _ptr(out_index), _ptr(out_count),
+                                           _stream(stream))
+    _check(st, "vico_temporal_drop")

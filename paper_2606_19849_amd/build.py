@@ -13,7 +13,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libvico.so")
-SOURCES = ["attn_fwd.hip", "attn_merge.hip", "attn_gather.hip", "retrieve.hip", "kv_append.hip", "vico_api.hip"]
+SOURCES = ["attn_fwd.hip", "attn_merge.hip", "attn_gather.hip", "retrieve.hip", "token_drop.hip", "kv_append.hip", "vico_api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -465,4 +465,44 @@ int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const voi
   return e == hipSuccess ? VICO_OK : hip_fail(e);
 }
 
+int vico_temporal_drop(const void* frames, int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
+                       int32_t feat_dim, float tau, const void* prev_frame, uint8_t* keep, float* sim,
+                       void* out_tokens, int32_t* out_index, int32_t* out_count, void* stream) {
+  if (num_chunks < 0 || frames_per_chunk < 1 || frames_per_chunk > 8 || tokens_per_frame < 1 || feat_dim < 8 ||
+      feat_dim % 8 != 0 || isnan(tau))
+    return VICO_ERR_INVALID_ARG;
+  const int64_t rows = int64_t(num_chunks) * frames_per_chunk * tokens_per_frame;
+  if (rows >= (int64_t(1) << 31)) return VICO_ERR_INVALID_ARG;
+  if (num_chunks == 0) return VICO_OK;
+  if (!frames || !keep || !out_index || !out_count) return VICO_ERR_INVALID_ARG;
+  if (!aligned16(frames) || (prev_frame && !aligned16(prev_frame)) || (out_tokens && !aligned16(out_tokens)) ||
+      !aligned_to(sim, 4) || !aligned_to(out_index, 4) || !aligned_to(out_count, 4))
+    return VICO_ERR_MISALIGNED;
+  const int64_t fb = rows * feat_dim * 2, pb = prev_frame ? int64_t(tokens_per_frame) * feat_dim * 2 : 0;
+  const int64_t kb = int64_t(num_chunks) * tokens_per_frame;
+  const void* outs[] = {keep, sim, out_tokens, out_index, out_count};
+  const int64_t outb[] = {kb, sim ? kb * 4 : 0, out_tokens ? fb : 0, rows * 4, 4};
+  for (int i = 0; i < 5; ++i) {
+    if (!outs[i]) continue;
+    if (overlaps(outs[i], outb[i], frames, fb) || overlaps(outs[i], outb[i], prev_frame, pb)) return VICO_ERR_INVALID_ARG;
+    for (int j = i + 1; j < 5; ++j)
+      if (outs[j] && overlaps(outs[i], outb[i], outs[j], outb[j])) return VICO_ERR_INVALID_ARG;
+  }
+  vico::DropArgs a{};
+  a.frames = (const uint16_t*)frames;
+  a.prev = frames_per_chunk == 1 ? (const uint16_t*)prev_frame : nullptr;
+  a.keep = keep;
+  a.sim = sim;
+  a.out = (uint16_t*)out_tokens;
+  a.out_index = out_index;
+  a.out_count = out_count;
+  a.B = num_chunks;
+  a.C = frames_per_chunk;
+  a.n_f = tokens_per_frame;
+  a.dm = feat_dim;
+  a.tau = tau;
+  const hipError_t e = vico::launch_temporal_drop(a, (hipStream_t)stream);
+  return e == hipSuccess ? VICO_OK : hip_fail(e);
+}
+
 }  // extern "C"

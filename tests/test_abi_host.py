@@ -16,7 +16,7 @@ MIS = 0x10008
 EXPECTED = {"vico_kv_append", "vico_chunk_prefill_attn", "vico_attn_plan", "vico_attn_workspace_bytes",
             "vico_status_str", "vico_last_hip_error", "vico_token_mean", "vico_chunk_scores", "vico_topk_chunks",
             "vico_gather_plan", "vico_gather_attn", "vico_chunk_prefill_attn_ex", "vico_attn_plan_ex",
-            "vico_acn_window"}
+            "vico_acn_window", "vico_temporal_drop"}
 
 
 def test_header_declares_the_expected_entry_points():
@@ -304,3 +304,26 @@ def test_balanced_plan_counts_whole_chunks_when_bidirectional():
     causal = vico.vico_attn_plan(**c)
     bidir = vico.vico_attn_plan(**c, flags=vico.VICO_ATTN_BIDIRECTIONAL)
     assert bidir[0] >= causal[0] >= 1
+
+
+def _drop(**kw):
+    a = dict(fr=A, B=2, C=4, nf=24, dm=64, tau=0.9, prev=None, keep=B, sim=B + 0x1000, out=B + 0x10000,
+             idx=B + 0x100000, cnt=B + 0x200000)
+    a.update(kw)
+    return lib.vico_temporal_drop(a["fr"], a["B"], a["C"], a["nf"], a["dm"], a["tau"], a["prev"], a["keep"],
+                                  a["sim"], a["out"], a["idx"], a["cnt"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(C=0), -1), (dict(C=9), -1), (dict(nf=0), -1), (dict(dm=60), -1), (dict(B=-1), -1),
+    (dict(tau=float("nan")), -1), (dict(fr=None), -1), (dict(keep=None), -1), (dict(idx=None), -1),
+    (dict(cnt=None), -1), (dict(fr=MIS), -4), (dict(out=B + 0x10008), -4), (dict(idx=B + 0x100002), -4),
+    (dict(keep=A + 0x100), -1),              # keep inside the frames
+    (dict(out=B + 0x800), -1),               # out_tokens over sim
+])
+def test_temporal_drop_rejects_bad_arguments(kw, status):
+    assert _drop(**kw) == status
+
+
+def test_temporal_drop_of_no_chunks_is_a_no_op():
+    assert _drop(B=0) == 0
