@@ -13,7 +13,7 @@ Default workload: one Qwen2.5-VL-7B-shaped attention layer -- 28 query /
 the >= 50 % of bf16 MFMA peak target is stated on.  `--workload` selects the
 others (3b, full, full_bounded, stream, append, and the query-side path:
 query = retrieval + attention over the retrieved chunks, decode = one
-decode step over them).
+decode step over them; drop = temporal token dropping of a batch of chunks).
 
 Prints one JSON line.  `value` is algorithmic TFLOP/s over whole steps
 (attention + append); `roofline` prices the attention kernel alone from
@@ -37,7 +37,8 @@ PEAK_HBM_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SRC = {"attn_fwd_kernel<128>": "paper_2606_19849_amd/csrc/attn_fwd.hip",
               "attn_gather_kernel<128>": "paper_2606_19849_amd/csrc/attn_gather.hip",
-              "kv_append_kernel": "paper_2606_19849_amd/csrc/kv_append.hip"}
+              "kv_append_kernel": "paper_2606_19849_amd/csrc/kv_append.hip",
+              "drop_sim_kernel<4>": "paper_2606_19849_amd/csrc/token_drop.hip"}
 
 
 def measured_traffic(kernel, workload):
@@ -78,6 +79,8 @@ DESCR = {
              "(256..1024 tokens each) + causal query; 28q/4kv, d128; 8 queries in rotation",
     "decode": "qwen2.5-vl-7b decode step per layer: 1 query row over sink 64 + 32 retrieved chunks + 64 tail "
               "tokens; 28q/4kv, d128; 8 retrieved sets in rotation",
+    "drop": "temporal token dropping, qwen2.5-vl-7b projector output: 16 chunks x 4 frames x 256 tokens x 3584, "
+            "tau 0.9, half the positions static; 4 input batches in rotation",
 }
 
 
@@ -370,6 +373,56 @@ def run_query_workload(args, torch, vico):
     return res
 
 
+def run_drop_workload(args, torch, vico):
+    """Temporal token dropping of a batch of chunks (HBM bound): algorithmic
+    bytes = the frames read once + the retained tokens and their indices
+    written once."""
+    from synth import make_drop_frames
+    B, C, n_f, dm, tau = 16, 4, 256, 3584, 0.9
+    n_batches = 4
+    batches = [_dev(torch, make_drop_frames(B, C, n_f, dm, seed=j)) for j in range(n_batches)]
+    keep = torch.empty((B, n_f), dtype=torch.uint8, device="cuda")
+    idx = torch.empty(B * C * n_f, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    out = torch.empty((B * C * n_f, dm), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+    kept = []
+    for fr in batches:
+        vico.vico_temporal_drop(fr, tau, keep, idx, cnt, out_tokens=out, stream=stream)
+        torch.cuda.synchronize()
+        kept.append(int(cnt.item()))
+    for j in range(args.warmup):
+        vico.vico_temporal_drop(batches[j % n_batches], tau, keep, idx, cnt, out_tokens=out, stream=stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for j in range(args.steps):
+        ev[j][0].record(stream)
+        vico.vico_temporal_drop(batches[(args.warmup + j) % n_batches], tau, keep, idx, cnt, out_tokens=out,
+                                stream=stream)
+        ev[j][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    n_keep = np.array([kept[(args.warmup + j) % n_batches] for j in range(args.steps)], dtype=np.float64)
+    in_bytes = B * C * n_f * dm * 2
+    alg = in_bytes + n_keep * (dm * 2 + 4) + B * n_f
+    gbs = float(np.mean(alg / (ms * 1e-3)) / 1e9)
+    return {
+        "metric": "temporal token dropping throughput (input tokens/s)",
+        "value": round(B * C * n_f * args.steps / elapsed, 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": DESCR["drop"], "retention": round(float(n_keep.mean()) / (B * C * n_f), 4)},
+        "call_us_mean": round(float(ms.mean()) * 1e3, 2),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": measured_traffic("drop_sim_kernel<4>", "drop"),
+                     "kernel": "drop_sim_kernel<4> + drop_compact_kernel",
+                     "bytes_per_launch_mean": float(alg.mean())},
+    }
+
+
 def run_append_workload(args, torch, vico):
     """Ring append at capacity (chunk = ring = 16384 tokens of the 7B shape): HBM roofline
     of the append kernel, which is also a plain copy of known size."""
@@ -414,7 +467,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append", "query", "decode"])
+    ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append", "query", "decode",
+                                                          "drop"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--traffic-bytes", type=float, default=None,
@@ -437,6 +491,8 @@ def main():
         res = run_append_workload(args, torch, vico)
     elif args.workload in ("query", "decode"):
         res = run_query_workload(args, torch, vico)
+    elif args.workload == "drop":
+        res = run_drop_workload(args, torch, vico)
     else:
         res = run_chunk_workload(args, torch, vico)
     print(json.dumps(res), flush=True)

@@ -14,7 +14,7 @@
 //                        in fp32, reduces them across the wave, and takes the
 //                        decision in fp32 (the similarity it reports is the one
 //                        the decision used).  HBM bound: reads the frames once.
-//   drop_compact_kernel  one work-group per (chunk, 32-position tile): ranks
+//   drop_compact_kernel  one work-group per (chunk, 4-position tile): ranks
 //                        its kept positions (counts of earlier chunks and
 //                        positions, then a scan of the tile) and copies the
 //                        retained token rows to their place in stream order.
@@ -27,7 +27,7 @@ namespace vico {
 namespace {
 
 constexpr int kDropThreads = 256;
-constexpr int kCompactTile = 32;      // positions per compaction work-group
+constexpr int kCompactTile = 4;       // positions per compaction work-group (up to 32 rows to copy)
 
 __device__ __forceinline__ float wave_sum64(float v) {
 #pragma unroll
@@ -144,6 +144,7 @@ __global__ __launch_bounds__(kDropThreads) void drop_compact_kernel(DropArgs a) 
   __shared__ int buf[kDropThreads / 64];
   __shared__ int row_src[8 * kCompactTile];     // flat source row of each retained token of the tile
   __shared__ int row_dst[8 * kCompactTile];
+  static_assert(kCompactTile <= kDropThreads, "one thread per tile position");
   const int tid = threadIdx.x;
   const int tiles = (a.n_f + kCompactTile - 1) / kCompactTile;
   const int b = blockIdx.x / tiles;
@@ -183,11 +184,26 @@ __global__ __launch_bounds__(kDropThreads) void drop_compact_kernel(DropArgs a) 
   const int n_rows = anchor * np + m * tile_cnt;
   for (int i = tid; i < n_rows; i += kDropThreads) a.out_index[row_dst[i]] = row_src[i];
   if (a.out) {
-    const int ch = a.dm / 8;                     // 16-byte pieces per row
-    for (int64_t i = tid; i < (int64_t)n_rows * ch; i += kDropThreads) {
-      const int row = (int)(i / ch), c8 = (int)(i % ch);
-      *(u32x4*)(a.out + (int64_t)row_dst[row] * a.dm + c8 * 8) =
-          *(const u32x4*)(a.frames + (int64_t)row_src[row] * a.dm + c8 * 8);
+    // one wave per row; each lane loads all its 16-byte pieces of the row
+    // (up to 8) before storing any, so a row's loads are in flight together
+    const int ch = a.dm / 8;
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int row = wave; row < n_rows; row += kDropThreads / 64) {
+      const u32x4* __restrict__ src = (const u32x4*)(a.frames + (int64_t)row_src[row] * a.dm);
+      u32x4* __restrict__ dst = (u32x4*)(a.out + (int64_t)row_dst[row] * a.dm);
+      for (int c0 = 0; c0 < ch; c0 += 8 * 64) {
+        u32x4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int c = c0 + k * 64 + lane;
+          if (c < ch) v[k] = src[c];
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int c = c0 + k * 64 + lane;
+          if (c < ch) dst[c] = v[k];
+        }
+      }
     }
   }
   if (b == a.B - 1 && p0 + np == a.n_f && tid == 0)
