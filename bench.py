@@ -35,23 +35,31 @@ PEAK_HBM_GBS = 8000.0
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SRC = {"attn_fwd_kernel<128>": "paper_2606_19849_amd/csrc/attn_fwd.hip",
-              "attn_gather_kernel<128>": "paper_2606_19849_amd/csrc/attn_gather.hip",
-              "kv_append_kernel": "paper_2606_19849_amd/csrc/kv_append.hip",
-              "drop_sim_kernel<4>": "paper_2606_19849_amd/csrc/token_drop.hip"}
+CSRC = "paper_2606_19849_amd/csrc/"
+# sources whose kernels a traffic figure covers (it goes stale when any changes)
+KERNEL_SRC = {"attn_fwd_kernel<128>": [CSRC + "attn_fwd.hip", CSRC + "attn_common.h"],
+              "attn_gather_kernel<128>": [CSRC + "attn_gather.hip", CSRC + "attn_merge.hip", CSRC + "attn_common.h"],
+              "kv_append_kernel": [CSRC + "kv_append.hip"],
+              "drop_sim_kernel<4>": [CSRC + "token_drop.hip"]}
+
+
+def kernel_source_sha256(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SRC[kernel]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()
 
 
 def measured_traffic(kernel, workload):
     """HBM bytes per launch from the committed rocprofv3 summary of this kernel and
     workload, or None when there is none or the kernel source changed since."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path):
         return None
     fields = dict(line.split(":", 1) for line in open(path) if ":" in line and not line.startswith("#"))
     fields = {k.strip(): v.strip() for k, v in fields.items()}
-    src = open(os.path.join(ROOT, KERNEL_SRC[kernel]), "rb").read()
-    if fields.get("kernel") != kernel or fields.get("kernel_source_sha256") != hashlib.sha256(src).hexdigest():
+    if fields.get("kernel") != kernel or fields.get("kernel_source_sha256") != kernel_source_sha256(kernel):
         return None
     return float(fields["hbm_bytes_per_launch"])
 
