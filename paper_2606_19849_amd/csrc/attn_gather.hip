@@ -39,21 +39,21 @@ namespace vico {
 namespace {
 
 template <int D>
-__global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherArgs a) {
+__global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherArgs a) {
   constexpr int BN = 64;
-  constexpr int BM = kBlockM;
+  constexpr int BM = kGatherThreads / 64 * 32;
   constexpr int NKS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int UPR = D / 8;
   constexpr int RBY = D * 2;
   constexpr int KT = BN * D;
-  constexpr int NW = kThreads / 64;
+  constexpr int NW = kGatherThreads / 64;
   constexpr int NLD = BN * RBY / 1024 / NW;
   constexpr int RPL = 1024 / RBY;
-  constexpr int SEG_PER_THREAD = kMaxSegments / kThreads;
+  constexpr int SEG_PER_THREAD = kMaxSegments / kGatherThreads;
   static_assert(NLD * NW * 1024 == BN * RBY, "direct loads cover the tile");
   static_assert(BM == NW * 32, "one 32-row block per wave");
-  static_assert(SEG_PER_THREAD * kThreads == kMaxSegments, "segment table split");
+  static_assert(SEG_PER_THREAD * kGatherThreads == kMaxSegments, "segment table split");
   auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
   auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
 
@@ -444,9 +444,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_gather_kernel(GatherA
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream) {
   const int grid = a.n_rt * a.parts * a.Hkv;
   if (a.D == 128)
-    hipLaunchKernelGGL(attn_gather_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(attn_gather_kernel<128>, dim3(grid), dim3(kGatherThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_gather_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(attn_gather_kernel<64>, dim3(grid), dim3(kGatherThreads), 0, stream, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || a.parts == 1) return err;
   AttnArgs m{};

@@ -154,7 +154,8 @@ int check_gather_shape(int32_t Lq, int32_t T, int32_t S, int32_t cap, int32_t n_
   const int g = Hq / Hkv;
   sh->Lq = Lq; sh->T = T; sh->S = S; sh->cap = cap; sh->n_segs = n_segs;
   sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;
-  sh->n_rt = (int)((int64_t(g) * Lq + vico::kBlockM - 1) / vico::kBlockM);
+  constexpr int kGatherRows = vico::kGatherThreads / 64 * 32;
+  sh->n_rt = (int)((int64_t(g) * Lq + kGatherRows - 1) / kGatherRows);
   const int64_t tiles = (S + std::min<int64_t>(hint, kMaxKeys) + T + vico::kKeyTile - 1) / vico::kKeyTile;
   int parts = 1;
   if (splits > 0) {

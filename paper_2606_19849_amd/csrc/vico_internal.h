@@ -47,6 +47,7 @@ struct AttnArgs {
 
 // Short-query attention over gathered key segments: query rows are the last
 // Lq of T tail tokens; keys = sink ++ store segments ++ tail (causal).
+constexpr int kGatherThreads = 512;  // 8 waves x 32 packed rows per work-group
 constexpr int kMaxSegments = 2048;   // segment table entries per call
 constexpr int kMaxGatherParts = 64;  // key-range parts per row tile
 struct GatherArgs {
