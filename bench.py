@@ -118,6 +118,34 @@ def _dev(torch, bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
 
+def sustained_mfma_tflops(torch, stream, iters=2000, reps=5):
+    """bf16 matrix-core rate the GPU sustains with every CU busy (register-only
+    MFMA chains, two waves per SIMD; libvico_bench.so), median of `reps` timed
+    launches on `stream`, in TFLOP/s.  Context for `roofline.peak`, which is the
+    published figure at the 2.4 GHz peak engine clock."""
+    import ctypes
+    from paper_2606_19849_amd.build import BENCH_LIB
+    lib = ctypes.CDLL(BENCH_LIB)
+    fn = lib.vico_bench_mfma_peak
+    fn.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int32
+    groups = torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.empty(groups * 8, dtype=torch.float32, device="cuda")
+    ms = []
+    for r in range(reps + 2):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        st = fn(groups, iters, sink.data_ptr(), stream.cuda_stream)
+        b.record(stream)
+        if st != 0:
+            raise RuntimeError(f"vico_bench_mfma_peak failed ({st})")
+        torch.cuda.synchronize()
+        if r >= 2:
+            ms.append(a.elapsed_time(b))
+    flops = groups * 8 * iters * 32 * 32768
+    return flops / (float(np.median(ms)) * 1e-3) / 1e12
+
+
 def run_chunk_workload(args, torch, vico):
     from synth import make_chunk_inputs
     sh = workload_shape(args.workload)
@@ -198,6 +226,9 @@ def run_chunk_workload(args, torch, vico):
                      "kernel": "attn_fwd_kernel<128>",
                      "flops_per_launch": fl},
     }
+    sustained = sustained_mfma_tflops(torch, stream)
+    res["roofline"]["sustained_peak"] = round(sustained, 1)
+    res["roofline"]["frac_of_sustained"] = round(achieved / sustained, 4)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_rows)
     return res

@@ -1,4 +1,5 @@
-"""Compile libvico.so (HIP kernels + C ABI) for gfx950, in-tree.
+"""Compile libvico.so (HIP kernels + C ABI) and the measurement helper
+libvico_bench.so for gfx950, in-tree.
 
 Usage: python -m paper_2606_19849_amd.build   (or build() from Python)
 """
@@ -14,6 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libvico.so")
 SOURCES = ["attn_fwd.hip", "attn_merge.hip", "attn_gather.hip", "retrieve.hip", "token_drop.hip", "kv_append.hip", "vico_api.hip"]
+BENCH_LIB = os.path.join(PKG, "libvico_bench.so")
+BENCH_SOURCES = ["mfma_peak.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -32,9 +35,15 @@ FLAGS = [
 
 
 def build(verbose: bool = False, extra_flags=()) -> str:
-    """Compile every HIP source into paper_2606_19849_amd/libvico.so; return its path."""
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
+    """Compile libvico.so and libvico_bench.so; return the path of libvico.so."""
+    _compile(SOURCES, LIB, verbose, extra_flags)
+    _compile(BENCH_SOURCES, BENCH_LIB, verbose, extra_flags)
+    return LIB
+
+
+def _compile(sources, lib, verbose, extra_flags) -> None:
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = lib + ".tmp"
     cmd = [HIPCC, *FLAGS, *extra_flags, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -51,9 +60,8 @@ def build(verbose: bool = False, extra_flags=()) -> str:
     nm = subprocess.run(["nm", "-u", tmp], capture_output=True, text=True)
     missing = [l.split()[-1] for l in nm.stdout.splitlines() if "__device_stub__" in l]
     if missing:
-        raise RuntimeError(f"libvico.so references kernel stubs that were not emitted: {missing}")
-    os.replace(tmp, LIB)
-    return LIB
+        raise RuntimeError(f"{os.path.basename(lib)} references kernel stubs that were not emitted: {missing}")
+    os.replace(tmp, lib)
 
 
 if __name__ == "__main__":

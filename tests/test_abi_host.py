@@ -327,3 +327,31 @@ def test_temporal_drop_rejects_bad_arguments(kw, status):
 
 def test_temporal_drop_of_no_chunks_is_a_no_op():
     assert _drop(B=0) == 0
+
+
+# ---- measurement helper library (libvico_bench.so, include/vico_bench.h)
+
+def _bench_header_functions():
+    import re
+    from paper_2606_19849_amd.build import INCLUDE
+    src = open(f"{INCLUDE}/vico_bench.h").read()
+    src = re.sub(r"//[^\n]*", "", src)
+    return sorted(set(re.findall(r"\b(vico_\w+)\s*\(", src)))
+
+
+def test_bench_library_exports_its_header():
+    from paper_2606_19849_amd.build import BENCH_LIB
+    blib = ctypes.CDLL(BENCH_LIB)
+    names = _bench_header_functions()
+    assert names == ["vico_bench_mfma_peak"]
+    for n in names:
+        assert hasattr(blib, n)
+
+
+@pytest.mark.parametrize("groups,iters,sink", [(0, 10, A), (4, 0, A), (4, 10, None), (-1, 10, A)])
+def test_bench_mfma_peak_rejects_bad_arguments(groups, iters, sink):
+    from paper_2606_19849_amd.build import BENCH_LIB
+    fn = ctypes.CDLL(BENCH_LIB).vico_bench_mfma_peak
+    fn.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int32
+    assert fn(groups, iters, sink, None) == -1      # VICO_ERR_INVALID_ARG, before any HIP call
