@@ -19,6 +19,9 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kNumXcd = 8;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
+// Largest lane sum of one half's probabilities accepted against the running
+// max: it bounds each term by 2^8, the headroom kRescaleThreshold gives.
+constexpr float kLaneSumLimit = 256.0f;
 
 // Logical work-group id for physical id `pid` so that each XCD receives a
 // contiguous block of logical ids (hardware dispatches ids round-robin over

@@ -25,9 +25,11 @@
 //     in the layout "lane = query row", so per-row rescale factors are
 //     lane-local.
 //   * Online softmax in fp32 with exp2 (v_exp_f32), scale*log2(e) folded into
-//     one FMA per logit.  The running max is only raised (and O rescaled)
-//     when some row's tile max exceeds it by more than 2^8; until then the
-//     probabilities are exp2 of at most 8, exact in fp32 and bf16 range.
+//     one FMA per logit.  Each half is exponentiated against the running max
+//     straight away; the max is only raised (and O rescaled, the half redone)
+//     when some lane's sum of probabilities exceeds 2^8, which bounds every
+//     probability by 2^8, or while a row has no max yet.  So no row-max
+//     reduction sits between the logits and the exponentials.
 //   * K/V tiles: 64 keys, double-buffered in LDS; the next tile's loads
 //     are in flight while the current tile is multiplied.  Loads go through
 //     buffer resources (one per sink / ring / chunk tensor): a tile that lies
@@ -290,51 +292,55 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
         if (kk > key_lim[rb]) s[rb][v] = -INFINITY;
       }
   };
-  // row maxima of one half (scaled to log2 units); true if some row grew by more than 2^8
-  auto max_half = [&](f32x16 (&s)[RB], float (&mx)[RB]) __attribute__((always_inline)) {
-    bool grow = false;
+  // Softmax of one half.  The probabilities are taken against the running
+  // max first (exp2, bf16 pack, lane sums), so the exponentials do not wait
+  // for a row-max reduction.  While no probability of the wave exceeds 2^8 (a
+  // lane's sum bounds each of its 16 terms) that max stays; otherwise, and
+  // while a row has no max yet, the max is raised to the half's row max, O and
+  // l are rescaled and the half is exponentiated again (rare, wave-uniform).
+  auto softmax_half = [&](const f32x16 (&s)[RB], bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
+    float lsum[RB];
+    auto expo = [&](int rb) __attribute__((always_inline)) {
+      const float neg_m = (m_run[rb] == -INFINITY) ? 0.f : -m_run[rb];
+      float e[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][v], c, neg_m));
+      float s0 = 0.f, s1 = 0.f;      // two chains
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        s0 += e[2 * v];
+        s1 += e[2 * v + 1];
+      }
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pf[rb][kp][j] = (__bf16)e[kp * 8 + j];
+      lsum[rb] = s0 + s1;
+    };
+    bool redo = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      float m = -INFINITY;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) m = fmaxf(m, s[rb][v]);
-      mx[rb] = pair_max(m) * c;
-      grow |= mx[rb] > m_run[rb] + kRescaleThreshold;
+      expo(rb);
+      redo |= !(lsum[rb] <= kLaneSumLimit) || m_run[rb] == -INFINITY;
     }
-    return grow;
-  };
-  // rare: raise the running max and rescale O and l (wave-uniform branch)
-  auto rescale = [&](bool grow, const float (&mx)[RB]) __attribute__((always_inline)) {
-    if (__builtin_amdgcn_ballot_w64(grow)) {
+    if (__builtin_amdgcn_ballot_w64(redo)) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const float m_new = fmaxf(m_run[rb], mx[rb]);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[rb][v]);
+        // branch-free per lane: a divergent branch here would keep two copies of O
+        const float m_new = fmaxf(m_run[rb], pair_max(mx) * c);
         const float alpha = (m_new == m_run[rb]) ? 1.f : __builtin_amdgcn_exp2f(m_run[rb] - m_new);
         l_run[rb] *= alpha;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) o[rb][db] *= alpha;
         m_run[rb] = m_new;
+        expo(rb);
       }
     }
-  };
-  // exp2, row sums, bf16 pack of one half: pf[rb][kp] for the half's two 16-key steps
-  auto exp_half = [&](f32x16 (&s)[RB], bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const float m_use = (m_run[rb] == -INFINITY) ? 0.f : m_run[rb];
-      float lsum = 0.f;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][v], c, -m_use));
-        s[rb][v] = p;
-        lsum += p;
-      }
-      l_run[rb] += lsum;
-#pragma unroll
-      for (int kp = 0; kp < 2; ++kp)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pf[rb][kp][e] = (__bf16)s[rb][kp * 8 + e];
-    }
+    for (int rb = 0; rb < RB; ++rb) l_run[rb] += lsum[rb];
   };
   // O^T += V^T P^T for one half: every V^T fragment feeds each row block
   auto pv_half = [&](const uint16_t* Vs, int h, const bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
@@ -354,29 +360,25 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
 
   // One 64-key tile in two 32-key halves, ordered so that the matrix cores
   // multiply one half while the VALU exponentiates the other:
-  //   QK(0) | max(0) | [QK(1) with exp(0)] [PV(0) with max(1)] | exp(1) | PV(1)
+  //   QK(0) | [QK(1) with softmax(0)] [PV(0) with softmax(1)] | PV(1)
   // The wave raises its issue priority while it feeds the matrix cores, so of
   // the two waves sharing a SIMD the one with MFMAs ready goes first and the
   // other's softmax VALU work fills the MFMA shadow.
   auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
     f32x16 s0[RB], s1[RB];
-    float mx0[RB], mx1[RB];
     bf16x8 p0[RB][2], p1[RB][2];
     __builtin_amdgcn_s_setprio(1);
     qk_half(Ks, 0, s0);
     __builtin_amdgcn_s_setprio(0);
     if constexpr (MASK) mask_half(k0, s0);
-    rescale(max_half(s0, mx0), mx0);
     __builtin_amdgcn_s_setprio(1);
     qk_half(Ks, 1, s1);
-    exp_half(s0, p0);
+    softmax_half(s0, p0);
     pv_half(Vs, 0, p0);
     if constexpr (MASK) mask_half(k0 + 32, s1);
-    const bool grow1 = max_half(s1, mx1);
     __builtin_amdgcn_s_setprio(0);
-    rescale(grow1, mx1);
-    exp_half(s1, p1);
+    softmax_half(s1, p1);
     __builtin_amdgcn_s_setprio(1);
     pv_half(Vs, 1, p1);
     __builtin_amdgcn_s_setprio(0);
