@@ -18,9 +18,9 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kNumXcd = 8;
 constexpr uint32_t kOutOfRange = 0x80000000u;
-constexpr float kRescaleThreshold = 8.0f;   // log2 units
-// Largest lane sum of one half's probabilities accepted against the running
-// max: it bounds each term by 2^8, the headroom kRescaleThreshold gives.
+// Largest lane sum of one half's 16 probabilities accepted against the
+// running max; it bounds each of them by 2^8 (exp2 of at most 8), far inside
+// the fp32 and bf16 range.
 constexpr float kLaneSumLimit = 256.0f;
 
 // Logical work-group id for physical id `pid` so that each XCD receives a

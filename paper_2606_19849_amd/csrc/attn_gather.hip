@@ -286,37 +286,42 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
       if (kk > key_lim) s[v] = -INFINITY;
     }
   };
-  auto max_half = [&](const f32x16& s, float& mx) __attribute__((always_inline)) {
-    float m = -INFINITY;
+  // Softmax of one half against the running max, as in the chunk kernel:
+  // exponentiate first; raise the max (rescale O and l, redo the half) only
+  // when a lane's sum of its 16 probabilities exceeds 2^8 or the row has no
+  // max yet.
+  auto softmax_half = [&](const f32x16& s, bf16x8 (&pf)[2]) __attribute__((always_inline)) {
+    auto expo = [&]() __attribute__((always_inline)) {
+      const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
+      float e[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) m = fmaxf(m, s[v]);
-    mx = pair_max(m) * c;
-    return mx > m_run + kRescaleThreshold;
-  };
-  auto rescale = [&](bool grow, float mx) __attribute__((always_inline)) {
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float m_new = fmaxf(m_run, mx);
+      for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, neg_m));
+      float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        s0 += e[2 * v];
+        s1 += e[2 * v + 1];
+      }
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pf[kp][j] = (__bf16)e[kp * 8 + j];
+      return s0 + s1;
+    };
+    float lsum = expo();
+    if (__builtin_amdgcn_ballot_w64(!(lsum <= kLaneSumLimit) || m_run == -INFINITY)) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[v]);
+      const float m_new = fmaxf(m_run, pair_max(mx) * c);
       const float alpha = (m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) o[db] *= alpha;
       m_run = m_new;
-    }
-  };
-  auto exp_half = [&](f32x16& s, bf16x8 (&pf)[2]) __attribute__((always_inline)) {
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    float lsum = 0.f;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -m_use));
-      s[v] = p;
-      lsum += p;
+      lsum = expo();
     }
     l_run += lsum;
-#pragma unroll
-    for (int kp = 0; kp < 2; ++kp)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pf[kp][e] = (__bf16)s[kp * 8 + e];
   };
   auto pv_half = [&](const uint16_t* Vs, int h, const bf16x8 (&pf)[2]) __attribute__((always_inline)) {
 #pragma unroll
@@ -333,22 +338,18 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
   auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
     f32x16 s0, s1;
-    float mx0, mx1;
     bf16x8 p0[2], p1[2];
     __builtin_amdgcn_s_setprio(1);
     qk_half(Ks, 0, s0);
     __builtin_amdgcn_s_setprio(0);
     if constexpr (MASK) mask_half(k0, s0);
-    rescale(max_half(s0, mx0), mx0);
     __builtin_amdgcn_s_setprio(1);
     qk_half(Ks, 1, s1);
-    exp_half(s0, p0);
+    softmax_half(s0, p0);
     pv_half(Vs, 0, p0);
     if constexpr (MASK) mask_half(k0 + 32, s1);
-    const bool grow1 = max_half(s1, mx1);
     __builtin_amdgcn_s_setprio(0);
-    rescale(grow1, mx1);
-    exp_half(s1, p1);
+    softmax_half(s1, p1);
     __builtin_amdgcn_s_setprio(1);
     pv_half(Vs, 1, p1);
     __builtin_amdgcn_s_setprio(0);
