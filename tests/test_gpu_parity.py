@@ -92,6 +92,31 @@ def test_large_logits_stay_finite():
     check_f32(o, ref, lse, ref_lse, max_abs=5e-2, mean_abs=2e-3, lse_abs=1e-3)
 
 
+@pytest.mark.parametrize("splits", [1, 3, -1])
+def test_rising_logits_rescale_often(splits):
+    """Keys scaled by a ramp that rises along the window and into the chunk, so
+    the row maxima keep growing and the running max is raised again and again:
+    the kernels raise it only when a lane's sum of 16 probabilities exceeds
+    2^8 (or a row has none yet), which happens here both through single large
+    probabilities and through many moderately large ones.  Peaked rows, so the
+    bound of the large-logit test applies."""
+    sh = SMALL["gqa7_ragged"]
+    inp = make_chunk_inputs(sh, seed=107, family="F2")
+    def ramp(bits, lo, hi):
+        x = bf16_bits_to_f64(bits).astype(np.float32)
+        r = np.linspace(lo, hi, x.shape[0], dtype=np.float32)[:, None, None]
+        return f32_to_bf16_bits(x * r)
+    inp.hist_k = ramp(inp.hist_k, 0.25, 2.5)
+    inp.k_chunk = ramp(inp.k_chunk, 2.5, 3.5)
+    ref, ref_lse = oracle_result(inp)
+    dc = DeviceChunk(inp)
+    o, lse = dc.attention(torch.float32, num_splits=splits)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    check_f32(o, ref, lse, ref_lse, max_abs=5e-2, mean_abs=2e-3, lse_abs=1e-3)
+    o16, _ = dc.attention(torch.bfloat16, num_splits=splits)
+    assert np.max(np.abs(o16.astype(np.float64) - o)) <= 2e-2 * max(1.0, float(np.max(np.abs(o))))
+
+
 def test_split_counts_agree():
     """Every split count meets the oracle tolerance; results differ between split
     counts only by where the bf16 probabilities are rounded (each split keeps its
