@@ -7,7 +7,7 @@
 // its O_s slot may never have been written).
 //
 // Few parts (up to 8, the chunk prefill splits) over many rows: one thread
-// per 4 columns of a row walks the parts.  Many parts (up to 64, short
+// per 4 columns of a row loads all parts together.  Many parts (up to 64, short
 // queries): a thread walking them one by one is bound by load latency, so a
 // work-group of 256 threads takes RPB rows, and for each row PG groups of
 // threads take every PG-th part and D/4 threads the 4-float columns -- all
@@ -20,11 +20,11 @@ namespace vico {
 namespace {
 
 constexpr int kMergeThreads = 256;
-constexpr int kFewParts = 8;     // up to here one thread per (row, 4 columns) walks the parts
+constexpr int kFewParts = 8;     // up to here one thread per (row, 4 columns) loads all parts
 
 // Few parts, many rows (chunk prefill splits): one thread per (head, row,
-// 4-column group) walks the parts; neighbouring threads read neighbouring
-// columns, so every load is a full coalesced row.
+// 4-column group) reads every part's value at once; neighbouring threads
+// read neighbouring columns, so every load is a full coalesced row.
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs a) {
   constexpr int NQ = D / 4;
@@ -33,17 +33,27 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs
   if (idx >= n_rows * NQ) return;
   const int dq = (int)(idx % NQ);
   const int64_t hr = idx / NQ;
+  // every part's lse and O of this thread are loaded together (up to
+  // kFewParts, unrolled), so one memory latency covers the whole row
+  float ls[kFewParts];
+  f32x4 os[kFewParts];
+#pragma unroll
+  for (int s = 0; s < kFewParts; ++s) ls[s] = s < a.splits ? a.ws_lse[s * n_rows + hr] : -INFINITY;
+#pragma unroll
+  for (int s = 0; s < kFewParts; ++s)
+    // an empty part (lse = -inf) may never have written its O slot: not read
+    os[s] = ls[s] != -INFINITY ? *(const f32x4*)(a.ws_o + (s * n_rows + hr) * D + dq * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
   float mx = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, a.ws_lse[s * n_rows + hr]);
+#pragma unroll
+  for (int s = 0; s < kFewParts; ++s) mx = fmaxf(mx, ls[s]);
   const float m_use = (mx == -INFINITY) ? 0.f : mx;
   f32x4 acc{0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    const float ls = a.ws_lse[s * n_rows + hr];
-    if (ls == -INFINITY) continue;      // empty part: its O slot may never have been written
-    const float w = __builtin_amdgcn_exp2f(ls - m_use);
+#pragma unroll
+  for (int s = 0; s < kFewParts; ++s) {
+    const float w = ls[s] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ls[s] - m_use);
     wsum += w;
-    acc += w * *(const f32x4*)(a.ws_o + (s * n_rows + hr) * D + dq * 4);
+    acc += w * os[s];
   }
   acc *= wsum > 0.f ? 1.f / wsum : 0.f;
   const int row = (int)(hr % a.C);

@@ -38,6 +38,10 @@ SMALL = {
     # spread over many work-groups, ring read wrapping
     "balanced_many_parts": ChunkShape(8, 2, 128, 64, 4096, 4596, 4000, 600),
     "balanced_d64": ChunkShape(4, 1, 64, 16, 8192, 10000, 8000, 300),
+    # many heads: 168 and 144 (row tile, head) pairs, between half and all of
+    # the work-groups; ring read wrapping
+    "many_heads": ChunkShape(56, 8, 128, 16, 640, 900, 512, 520),
+    "many_heads_d64": ChunkShape(48, 6, 64, 9, 300, 777, 300, 700),
 }
 
 
@@ -132,6 +136,23 @@ def test_split_counts_agree():
         check_f32(o, ref, lse, ref_lse)
         assert np.max(np.abs(o - base)) <= 2e-2
         assert np.max(np.abs(lse - base_lse)) <= 2e-3
+
+
+@pytest.mark.parametrize("cfg", ["7b", "7b_wrap"])
+def test_balanced_schedule_agrees_on_every_row(cfg):
+    """Full 7B-shaped chunk: the balanced schedule (every work-group an equal
+    share of all key tiles; row tiles cut between work-groups and merged by
+    log-sum-exp) against the default one, on every row and head."""
+    import paper_2606_19849_amd as vico
+    sh = CONFIGS[cfg]
+    inp = make_chunk_inputs(sh, seed=108, family="F2")
+    dc = DeviceChunk(inp)
+    base, base_lse = dc.attention(torch.float32, num_splits=0)
+    bal, bal_lse = dc.attention(torch.float32, num_splits=vico.VICO_SPLIT_BALANCED)
+    assert np.all(np.isfinite(bal))
+    assert np.max(np.abs(bal - base)) <= 2e-2
+    assert np.mean(np.abs(bal - base)) <= 1e-3
+    assert np.max(np.abs(bal_lse - base_lse)) <= 2e-3
 
 
 def _sample_rows(C, n=40, seed=0):
