@@ -240,6 +240,57 @@ def test_decode_step(splits):
     check_f32(o, ro, l, rl)
 
 
+def test_decode_step_replays_as_a_graph():
+    """A decode step captured into a HIP graph (the library launches kernels
+    only: no memset, copy or allocation) replays the eager result exactly,
+    replay after replay, with other eager work of the same buffers between."""
+    qi = make_query_inputs(QUERY_CONFIGS["q_gqa7"], seed=15, family="F2")
+    sh = qi.shape
+    d = DeviceQuery(qi)
+    q = d.q[-1:].contiguous()
+    tables = [oracle.chunk_segments(np.array(c), qi.chunk_start, qi.chunk_len) for c in ([0, 5, 6, 20], [1, 2, 9])]
+    segs = [(torch.from_numpy(st.astype(np.int64)).cuda(), torch.from_numpy(ln.astype(np.int32)).cuda())
+            for st, ln in tables]
+    hint = max(int(ln.sum()) for _, ln in tables)
+    parts, wb = vico.vico_gather_plan(1, sh.tail_len, sh.sink_len, d.gk.shape[0], 4, hint, sh.num_q_heads,
+                                      sh.num_kv_heads, sh.head_dim)
+    assert parts > 1                  # the merge kernel is part of the graph
+    ws = torch.empty(wb, dtype=torch.uint8, device="cuda")
+    out = torch.empty((1, sh.num_q_heads, sh.head_dim), dtype=torch.float32, device="cuda")
+    lse = torch.empty((sh.num_q_heads, 1), dtype=torch.float32, device="cuda")
+
+    def step(i):
+        vico.vico_gather_attn(q, d.tk, d.tv, d.sk, d.sv, d.gk, d.gv, segs[i][0], segs[i][1], out, lse=lse,
+                              workspace=ws, keys_hint=hint)
+
+    eager = []
+    for i in range(2):
+        step(i)
+        torch.cuda.synchronize()
+        eager.append((out.clone(), lse.clone()))
+    ro, rl = d.reference(*tables[0], q_rows=1)
+    check_f32(eager[0][0].cpu().numpy().astype(np.float64), ro, eager[0][1].cpu().numpy().astype(np.float64), rl)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        step(0)                       # warm-up on the capture stream
+        torch.cuda.current_stream().synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            step(0)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        step(1)                       # eager call of another table, same buffers
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager[1][0]) and torch.equal(lse, eager[1][1])
+        out.zero_()
+        lse.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager[0][0]) and torch.equal(lse, eager[0][1])
+
+
 def test_no_segments_attends_sink_and_tail():
     qi = make_query_inputs(QUERY_CONFIGS["q_small"], seed=14, family="F2")
     d = DeviceQuery(qi)
