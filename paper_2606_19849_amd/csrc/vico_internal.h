@@ -20,7 +20,6 @@ constexpr int kNumCUs = 256;        // MI355X: 8 XCDs x 32 CUs
 constexpr int kWgPerCU = 1;
 constexpr int kMaxSplits = 16;
 
-inline int key_tile(int) { return kKeyTile; }
 
 // Everything the attention kernels need, resolved on the host.
 struct AttnArgs {
