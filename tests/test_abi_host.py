@@ -355,3 +355,16 @@ def test_bench_mfma_peak_rejects_bad_arguments(groups, iters, sink):
     fn.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     fn.restype = ctypes.c_int32
     assert fn(groups, iters, sink, None) == -1      # VICO_ERR_INVALID_ARG, before any HIP call
+
+
+def test_tensor_size_limit_is_2_to_the_31_bytes():
+    """K/V tensors are addressed through 32-bit buffer offsets: one d128 head of
+    2^23 - 1 ring or store slots is the largest accepted, 2^23 slots (exactly
+    2^31 bytes) is rejected."""
+    R = (1 << 23) - 1
+    assert vico.vico_attn_plan(64, 16, R, R + 777, R - 100000, 2, 1, 128)[0] >= 1
+    with pytest.raises(vico.VicoError):
+        vico.vico_attn_plan(64, 16, R + 1, R + 777, R - 100000, 2, 1, 128)
+    assert vico.vico_gather_plan(2, 64, 16, R, 3, 10000, 7, 1, 128)[0] >= 1
+    with pytest.raises(vico.VicoError):
+        vico.vico_gather_plan(2, 64, 16, R + 1, 3, 10000, 7, 1, 128)

@@ -187,3 +187,66 @@ def test_full_size_sampled_rows_f1_fp32(cfg):
     ref, ref_lse = oracle_result(inp, rows=rows)
     check_relative(o[rows], ref)
     assert np.max(np.abs(lse[:, rows] - ref_lse)) <= 1e-3
+
+
+def _slot_marks(slots):
+    """0/1 per ring slot from a multiplicative hash (pattern of the max-size test)."""
+    return ((slots * 2654435761) >> 13) & 1
+
+
+def test_ring_at_the_32bit_offset_limit():
+    """Largest ring the kernels address: 2^31 bytes per K/V tensor less one row
+    (8388607 slots of one d128 head).  Every key is zero, so every logit is 0:
+    a row's output is the plain mean of the V rows it sees and its LSE is
+    ln(count), a closed form of the attention definition.  Ring V rows carry a
+    slot-hashed 0/1 pattern, so a misaddressed, wrapped-wrong or out-of-range
+    read changes the mean.  The window leaves 100000 slots out and wraps at the
+    ring end; the slots nearest 2^31 bytes are read.  An append across the
+    ring end then lands bit-exact."""
+    import paper_2606_19849_amd as vico
+    Hq, Hkv, D, S, C = 2, 1, 128, 16, 64
+    R = (1 << 31) // (Hkv * D * 2) - 1
+    H = R + 777
+    W = R - 100000
+    dev = "cuda"
+    g = torch.Generator().manual_seed(7)
+    cvec = ((torch.arange(D) % 7 - 3) / 4).to(torch.bfloat16)            # exact in bf16
+    rk = torch.zeros((R, Hkv, D), dtype=torch.bfloat16, device=dev)
+    rv = (_slot_marks(torch.arange(R, device=dev)).to(torch.bfloat16)[:, None] * cvec.to(dev)[None, :])
+    rv = rv.reshape(R, Hkv, D)
+    sk = torch.zeros((S, Hkv, D), dtype=torch.bfloat16, device=dev)
+    sv = torch.randn((S, Hkv, D), generator=g).to(torch.bfloat16)
+    kc = torch.zeros((C, Hkv, D), dtype=torch.bfloat16, device=dev)
+    vc = torch.randn((C, Hkv, D), generator=g).to(torch.bfloat16)
+    q = torch.randn((C, Hq, D), generator=g).to(torch.bfloat16).to(dev)
+    ns, wb = vico.vico_attn_plan(C, S, R, H, W, Hq, Hkv, D)
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device=dev)
+    out = torch.empty((C, Hq, D), dtype=torch.float32, device=dev)
+    lse = torch.empty((Hq, C), dtype=torch.float32, device=dev)
+    vico.vico_chunk_prefill_attn(q, kc, vc.to(dev), sk, sv.to(dev), rk, rv, H, W, out, lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+
+    # visible ring slots: history tokens H-W .. H-1 live at slots (H-W+k) mod R
+    ws0 = (H - W) % R
+    vis = np.concatenate([np.arange(ws0, R), np.arange(0, (ws0 + W) - R)]) if ws0 + W > R else np.arange(ws0, ws0 + W)
+    assert vis.size == W and ws0 + W > R
+    ring_sum = float(_slot_marks(vis.astype(np.int64)).sum()) * cvec.double().numpy()
+    sv64, vc64 = sv.double().numpy()[:, 0], vc.double().numpy()[:, 0]
+    n = S + W + np.arange(C) + 1
+    mean = (sv64.sum(0)[None, :] + ring_sum[None, :] + np.cumsum(vc64, axis=0)) / n[:, None]
+    o = out.cpu().double().numpy()
+    for h in range(Hq):
+        assert np.max(np.abs(o[:, h] - mean)) <= 1e-4
+    assert np.max(np.abs(lse.cpu().double().numpy() - np.log(n)[None, :])) <= 1e-4
+
+    # append of 4096 tokens across the ring end
+    Ca = 4096
+    ka = torch.randn((Ca, Hkv, D), generator=g).to(torch.bfloat16).to(dev)
+    va = torch.randn((Ca, Hkv, D), generator=g).to(torch.bfloat16).to(dev)
+    p0 = R - 1000
+    before = rv[p0 - 1].clone(), rv[Ca - 1000].clone()
+    vico.vico_kv_append(ka, va, rk, rv, p0)
+    torch.cuda.synchronize()
+    assert torch.equal(rk[p0:], ka[:1000]) and torch.equal(rk[:Ca - 1000], ka[1000:])
+    assert torch.equal(rv[p0:], va[:1000]) and torch.equal(rv[:Ca - 1000], va[1000:])
+    assert torch.equal(rv[p0 - 1], before[0]) and torch.equal(rv[Ca - 1000], before[1])

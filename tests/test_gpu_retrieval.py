@@ -427,3 +427,46 @@ def test_query_path_full_size(name):
     # stage 4: attention over the selected chunks, every row and head
     ro, rl = d.reference(st, ln)
     check_f32(out.cpu().numpy().astype(np.float64), ro, lse.cpu().numpy().astype(np.float64), rl)
+
+
+def test_store_at_the_32bit_offset_limit():
+    """Largest store the gathered attention addresses (2^31 bytes per K/V
+    tensor less one row: 8388607 slots of one d128 head).  All keys are zero,
+    so each query row's output is the plain mean of the V rows it sees (sink,
+    segments, causal tail) and its LSE is ln(count).  Store V rows carry a
+    slot-hashed 0/1 pattern and the segments include the store's last slots,
+    so a misaddressed or out-of-range read changes the mean."""
+    Hq, Hkv, D, S, T, Lq = 7, 1, 128, 16, 64, 2
+    cap = (1 << 31) // (Hkv * D * 2) - 1
+    dev = "cuda"
+    g = torch.Generator().manual_seed(9)
+    marks = lambda x: ((x * 2654435761) >> 13) & 1
+    cvec = ((torch.arange(D) % 7 - 3) / 4).to(torch.bfloat16)
+    gk = torch.zeros((cap, Hkv, D), dtype=torch.bfloat16, device=dev)
+    gv = (marks(torch.arange(cap, device=dev)).to(torch.bfloat16)[:, None] * cvec.to(dev)[None, :]).reshape(cap, Hkv, D)
+    sk = torch.zeros((S, Hkv, D), dtype=torch.bfloat16, device=dev)
+    sv = torch.randn((S, Hkv, D), generator=g).to(torch.bfloat16)
+    tk = torch.zeros((T, Hkv, D), dtype=torch.bfloat16, device=dev)
+    tv = torch.randn((T, Hkv, D), generator=g).to(torch.bfloat16)
+    q = torch.randn((Lq, Hq, D), generator=g).to(torch.bfloat16).to(dev)
+    st = np.array([cap - 5000, 0, 4_000_000], np.int64)
+    ln = np.array([5000, 3000, 2000], np.int32)
+    hint = int(ln.sum())
+    parts, wb = vico.vico_gather_plan(Lq, T, S, cap, len(st), hint, Hq, Hkv, D)
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device=dev)
+    out = torch.empty((Lq, Hq, D), dtype=torch.float32, device=dev)
+    lse = torch.empty((Hq, Lq), dtype=torch.float32, device=dev)
+    vico.vico_gather_attn(q, tk, tv.to(dev), sk, sv.to(dev), gk, gv, torch.from_numpy(st).to(dev),
+                          torch.from_numpy(ln).to(dev), out, lse=lse, workspace=ws, keys_hint=hint)
+    torch.cuda.synchronize()
+    slots = np.concatenate([np.arange(a, a + n, dtype=np.int64) for a, n in zip(st, ln)])
+    seg_sum = float(marks(slots).sum()) * cvec.double().numpy()
+    sv64, tv64 = sv.double().numpy()[:, 0], tv.double().numpy()[:, 0]
+    o = out.cpu().double().numpy()
+    l = lse.cpu().double().numpy()
+    for i in range(Lq):
+        vis_tail = T - Lq + i + 1
+        n = S + hint + vis_tail
+        mean = (sv64.sum(0) + seg_sum + tv64[:vis_tail].sum(0)) / n
+        assert np.max(np.abs(o[i] - mean[None, :])) <= 1e-4
+        assert np.max(np.abs(l[:, i] - np.log(n))) <= 1e-4
