@@ -533,8 +533,8 @@ def main():
                     help="HBM bytes per attention launch from rocprofv3 FETCH_SIZE+WRITE_SIZE, if measured")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; the multi-GPU layout (KV-head sharding) is "
-              "described in the design notes but not built", file=sys.stderr)
+        print("bench.py: the library runs on one GPU only; sharding by KV-head group across GPUs is "
+              "a design, not built", file=sys.stderr)
         sys.exit(2)
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
     import torch
