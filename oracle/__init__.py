@@ -10,7 +10,7 @@ set of keys -- here a fixed sink prefix, the W most recent history tokens and
 the chunk itself under a causal mask -- instead of the whole accumulated
 history.  The visibility rules restate the vision rows of the additive mask of
 Eq. (4) at token granularity.  Readings where the paper is silent are listed
-in the module docstrings and in the design notes.
+in the module docstrings.
 
 Modules
   bf16       -- widen bfloat16 bit patterns to float64 exactly

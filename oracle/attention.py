@@ -6,8 +6,7 @@ V_hat are the keys and values the chunk may see.  The vision rows of the
 additive mask of Eq. (4) say which keys those are: recent visual history and
 the current chunk, everything else masked with -inf.
 
-Readings taken where the paper is silent or loose (each is also recorded in
-the design notes):
+Readings taken where the paper is silent or loose:
   * Window unit: the visible history is the W most recent history *tokens*
     (the token-granular "Nearest-K" context of the nearest-visual-context
     table), not whole chunks; W < 0 means the full history.

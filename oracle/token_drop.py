@@ -9,8 +9,7 @@ kept as an anchor.  With c = 1 the rule degenerates to frame-level dropping:
 a frame's token is dropped when its similarity to the same position of the
 previous frame exceeds tau, with no anchor.
 
-Readings taken where the paper is silent (each is also recorded in the
-design notes):
+Readings taken where the paper is silent:
   * A dropped position loses its tokens in frames 2..c; frame 1's token
     stays (the anchor).  A position that is not dropped keeps all c tokens.
   * Retained tokens keep stream order: chunk by chunk, frame by frame, and
