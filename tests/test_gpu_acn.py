@@ -32,6 +32,23 @@ def test_bidirectional_bf16(name):
     check_bf16(o, oracle_result(inp, bidirectional=True)[0])
 
 
+@pytest.mark.parametrize("cfg", ["7b_wrap", "3b_wrap"])
+def test_bidirectional_full_size_sampled_rows(cfg):
+    """Full 7B/3B-shaped chunk with every row seeing the whole chunk: all row
+    tiles then share one key count (the schedule differs from the causal one),
+    sampled rows of every row tile against the oracle, bf16 output and LSE."""
+    from synth import CONFIGS
+    sh = CONFIGS[cfg]
+    inp = make_chunk_inputs(sh, seed=5, family="F2")
+    o, lse = DeviceChunk(inp).attention(torch.bfloat16, flags=BIDIR)
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([rng.choice(sh.chunk_len, 24, replace=False),
+                                     [0, 255, 256, sh.chunk_len - 1]]))
+    ref, ref_lse = oracle_result(inp, rows=rows, bidirectional=True)
+    check_bf16(o[rows], ref)
+    assert np.max(np.abs(lse[:, rows] - ref_lse)) <= 1e-3
+
+
 @pytest.mark.parametrize("flags", [0, BIDIR])
 def test_acn_window_stream(flags):
     """32 ragged chunks (256..1024 tokens) at 3B heads with the window set to
