@@ -31,7 +31,7 @@ class DeviceChunk:
         self.rk = dev(rk) if sh.ring_slots else None
         self.rv = dev(rv) if sh.ring_slots else None
 
-    def attention(self, out_dtype=torch.float32, num_splits=0, with_lse=True, flags=0):
+    def attention(self, out_dtype=torch.float32, num_splits=0, with_lse=True, flags=0, scale=0.0):
         sh = self.inp.shape
         out = torch.empty((sh.chunk_len, sh.num_q_heads, sh.head_dim), dtype=out_dtype, device="cuda")
         lse = torch.empty((sh.num_q_heads, sh.chunk_len), dtype=torch.float32, device="cuda") if with_lse else None
@@ -40,15 +40,16 @@ class DeviceChunk:
         ws = torch.empty(wb, dtype=torch.uint8, device="cuda") if wb else None
         vico.vico_chunk_prefill_attn(self.q, self.kc, self.vc, self.sk, self.sv, self.rk, self.rv,
                                      sh.hist_len, sh.window, out, lse=lse, workspace=ws, num_splits=num_splits,
-                                     flags=flags)
+                                     softmax_scale=scale, flags=flags)
         torch.cuda.synchronize()
         o = out.float().cpu().numpy().astype(np.float64)
         l = lse.cpu().numpy().astype(np.float64) if with_lse else None
         return o, l
 
 
-def oracle_result(inp: ChunkInputs, rows=None, heads=None, bidirectional=False):
-    return oracle.chunk_prefill_attention(**to_f64(inp), rows=rows, heads=heads, bidirectional=bidirectional)
+def oracle_result(inp: ChunkInputs, rows=None, heads=None, bidirectional=False, scale=None):
+    return oracle.chunk_prefill_attention(**to_f64(inp), rows=rows, heads=heads, bidirectional=bidirectional,
+                                          scale=scale)
 
 
 def check_f32(o, ref, lse=None, ref_lse=None, max_abs=1e-2, mean_abs=1e-3, lse_abs=1e-3):

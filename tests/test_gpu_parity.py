@@ -121,6 +121,18 @@ def test_rising_logits_rescale_often(splits):
     assert np.max(np.abs(o16.astype(np.float64) - o)) <= 2e-2 * max(1.0, float(np.max(np.abs(o))))
 
 
+@pytest.mark.parametrize("scale", [0.05, 0.2, 1.0])
+@pytest.mark.parametrize("splits", [1, 3])
+def test_explicit_softmax_scale(scale, splits):
+    """softmax_scale > 0 replaces 1/sqrt(d).  F2 inputs put the logits' standard
+    deviation at ~45 * scale (d = 128): from soft (2.3) to nearly one-hot (45).
+    fp32 output and LSE against the oracle at the same scale."""
+    inp = make_chunk_inputs(SMALL["gqa7_ragged"], seed=109, family="F2")
+    o, lse = DeviceChunk(inp).attention(torch.float32, num_splits=splits, scale=scale)
+    ref, ref_lse = oracle_result(inp, scale=scale)
+    check_f32(o, ref, lse, ref_lse)
+
+
 def test_split_counts_agree():
     """Every split count meets the oracle tolerance; results differ between split
     counts only by where the bf16 probabilities are rounded (each split keeps its

@@ -291,6 +291,32 @@ def test_decode_step_replays_as_a_graph():
         assert torch.equal(out, eager[0][0]) and torch.equal(lse, eager[0][1])
 
 
+@pytest.mark.parametrize("scale", [0.03, 0.5])
+def test_gather_explicit_softmax_scale(scale):
+    """softmax_scale > 0 replaces 1/sqrt(d) on the gathered path too (4 query
+    rows, F2 inputs), fp32 output and LSE against the oracle at that scale."""
+    qi = make_query_inputs(QUERY_CONFIGS["q_gqa7"], seed=16, family="F2")
+    sh = qi.shape
+    st, ln = oracle.chunk_segments(np.array([1, 4, 7]), qi.chunk_start, qi.chunk_len)
+    d = DeviceQuery(qi)
+    Lq = 4
+    q = d.q[-Lq:].contiguous()
+    hint = int(ln.sum())
+    parts, wb = vico.vico_gather_plan(Lq, sh.tail_len, sh.sink_len, d.gk.shape[0], len(st), hint, sh.num_q_heads,
+                                      sh.num_kv_heads, sh.head_dim)
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+    out = torch.empty((Lq, sh.num_q_heads, sh.head_dim), dtype=torch.float32, device="cuda")
+    lse = torch.empty((sh.num_q_heads, Lq), dtype=torch.float32, device="cuda")
+    vico.vico_gather_attn(q, d.tk, d.tv, d.sk, d.sv, d.gk, d.gv, torch.from_numpy(st.astype(np.int64)).cuda(),
+                          torch.from_numpy(ln.astype(np.int32)).cuda(), out, lse=lse, workspace=ws,
+                          keys_hint=hint, softmax_scale=scale)
+    torch.cuda.synchronize()
+    k, v = d.store_np
+    ro, rl = oracle.gather_attention(f64(qi.q)[-Lq:], f64(qi.tail_k), f64(qi.tail_v), f64(qi.sink_k),
+                                     f64(qi.sink_v), f64(k), f64(v), st, ln, scale=scale)
+    check_f32(out.cpu().numpy().astype(np.float64), ro, lse.cpu().numpy().astype(np.float64), rl)
+
+
 def test_no_segments_attends_sink_and_tail():
     qi = make_query_inputs(QUERY_CONFIGS["q_small"], seed=14, family="F2")
     d = DeviceQuery(qi)
