@@ -133,6 +133,39 @@ def test_explicit_softmax_scale(scale, splits):
     check_f32(o, ref, lse, ref_lse)
 
 
+@pytest.mark.parametrize("splits", [1, 3])
+def test_no_lse_and_side_stream_give_the_same_output(splits):
+    """The LSE output is optional: without it the output is bit-identical
+    (also through the split merge).  The library runs on the caller's stream:
+    attention and append issued on a side stream give bit-identical results."""
+    import paper_2606_19849_amd as vico
+    inp = make_chunk_inputs(SMALL["gqa7_ragged"], seed=110, family="F2")
+    dc = DeviceChunk(inp)
+    o_lse, _ = dc.attention(torch.float32, num_splits=splits)
+    o_none, l_none = dc.attention(torch.float32, num_splits=splits, with_lse=False)
+    assert l_none is None and np.array_equal(o_lse, o_none)
+
+    sh = inp.shape
+    ring = [dc.rk.clone(), dc.rv.clone()]
+    outs = []
+    for stream in (torch.cuda.current_stream(), torch.cuda.Stream()):
+        stream.wait_stream(torch.cuda.current_stream())
+        rk, rv = ring[0].clone(), ring[1].clone()
+        out = torch.empty((sh.chunk_len, sh.num_q_heads, sh.head_dim), dtype=torch.float32, device="cuda")
+        _, wb = vico.vico_attn_plan(sh.chunk_len, sh.sink_len, sh.ring_slots, sh.hist_len, sh.window,
+                                    sh.num_q_heads, sh.num_kv_heads, sh.head_dim, splits)
+        ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+        with torch.cuda.stream(stream):
+            vico.vico_chunk_prefill_attn(dc.q, dc.kc, dc.vc, dc.sk, dc.sv, rk, rv, sh.hist_len, sh.window, out,
+                                         workspace=ws, num_splits=splits, stream=stream)
+            vico.vico_kv_append(dc.kc, dc.vc, rk, rv, sh.hist_len, stream=stream)
+        stream.synchronize()
+        outs.append((out.clone(), rk, rv))
+    assert torch.equal(outs[0][0], outs[1][0])
+    assert torch.equal(outs[0][1], outs[1][1]) and torch.equal(outs[0][2], outs[1][2])
+    assert np.array_equal(outs[0][0].cpu().numpy().astype(np.float64), o_lse)
+
+
 def test_split_counts_agree():
     """Every split count meets the oracle tolerance; results differ between split
     counts only by where the bf16 probabilities are rounded (each split keeps its
