@@ -70,8 +70,11 @@ def hold_gpu(torch, stream, cycles=10_000_000):
     that the host enqueues the calls faster than the GPU runs them: the events
     around each call then bracket its kernels rather than the Python call
     overhead that would otherwise pace an idle GPU."""
+    sleep = getattr(torch.cuda, "_sleep", None)
+    if sleep is None:       # without it the events stay host-paced (upper bounds on kernel time)
+        return
     with torch.cuda.stream(stream):
-        torch.cuda._sleep(cycles)
+        sleep(cycles)
 
 
 def attn_flops(C, S, Wv, Hq, D, rows=None):
