@@ -96,6 +96,8 @@ class ChunkInputs:
 
 
 def _draw(rng: np.random.Generator, shape, sigma: float) -> np.ndarray:
+    if sigma == "U":      # uniform in [-1, 1)
+        return f32_to_bf16_bits(rng.uniform(-1.0, 1.0, shape).astype(np.float32))
     return f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(sigma))
 
 
@@ -105,12 +107,16 @@ def make_chunk_inputs(shape: ChunkShape, seed=0, family: str = "F1") -> ChunkInp
     family "F1": Q, K, V ~ N(0,1)/sqrt(head_dim) (the literal workload recipe).
     family "F2": Q, K ~ 2*N(0,1), V ~ N(0,1): logits of standard deviation 4
                  and O(1) outputs, used for the binding parity tolerance.
+    family "F2U": Q, K as in F2, V uniform in [-1, 1): every output lies in
+                 [-1, 1], the literal reading of "O(1)-scaled outputs".
     """
     d = shape.head_dim
     if family == "F1":
         sq = sk = sv = 1.0 / np.sqrt(d)
     elif family == "F2":
         sq, sk, sv = 2.0, 2.0, 1.0
+    elif family == "F2U":
+        sq, sk, sv = 2.0, 2.0, "U"
     else:
         raise ValueError(f"unknown input family {family!r}")
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -232,6 +238,8 @@ class QueryInputs:
 
 
 def _family_sigmas(family: str, d: int):
+    if family == "F2U":
+        return 2.0, 2.0, "U"
     if family == "F1":
         return (1.0 / np.sqrt(d),) * 3
     if family == "F2":

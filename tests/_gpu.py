@@ -8,6 +8,7 @@ import torch
 import oracle
 import paper_2606_19849_amd as vico
 from synth import ChunkInputs
+from tests._bounds import U8, Bound, chunk_bound
 from tests._util import ring_from_inputs, to_f64
 
 
@@ -35,8 +36,8 @@ class DeviceChunk:
         sh = self.inp.shape
         out = torch.empty((sh.chunk_len, sh.num_q_heads, sh.head_dim), dtype=out_dtype, device="cuda")
         lse = torch.empty((sh.num_q_heads, sh.chunk_len), dtype=torch.float32, device="cuda") if with_lse else None
-        _, wb = vico.vico_attn_plan(sh.chunk_len, sh.sink_len, sh.ring_slots, sh.hist_len, sh.window,
-                                    sh.num_q_heads, sh.num_kv_heads, sh.head_dim, num_splits, flags)
+        self.parts, wb = vico.vico_attn_plan(sh.chunk_len, sh.sink_len, sh.ring_slots, sh.hist_len, sh.window,
+                                             sh.num_q_heads, sh.num_kv_heads, sh.head_dim, num_splits, flags)
         ws = torch.empty(wb, dtype=torch.uint8, device="cuda") if wb else None
         vico.vico_chunk_prefill_attn(self.q, self.kc, self.vc, self.sk, self.sv, self.rk, self.rv,
                                      sh.hist_len, sh.window, out, lse=lse, workspace=ws, num_splits=num_splits,
@@ -52,31 +53,53 @@ def oracle_result(inp: ChunkInputs, rows=None, heads=None, bidirectional=False, 
                                           scale=scale)
 
 
-def check_f32(o, ref, lse=None, ref_lse=None, max_abs=1e-2, mean_abs=1e-3, lse_abs=1e-3):
-    """Binding tolerance on O(1)-scaled outputs (fp32 output path).
+def oracle_and_bound(inp: ChunkInputs, rows=None, heads=None, bidirectional=False, scale=None, parts=1,
+                     sigma=False, exact_dot=False):
+    """Oracle output and LSE with the derived per-element bound (tests/_bounds.py)."""
+    x = to_f64(inp)
+    ref, ref_lse = oracle.chunk_prefill_attention(**x, rows=rows, heads=heads, bidirectional=bidirectional,
+                                                  scale=scale)
+    b = chunk_bound(x, rows=rows, heads=heads, bidirectional=bidirectional, scale=scale, parts=parts,
+                    sigma=sigma, exact_dot=exact_dot)
+    return ref, ref_lse, b
 
-    The probabilities are rounded to bf16 (relative error up to 2^-9 per
-    weight), so an output's error carries the size of the values it averages;
-    the max-abs bound applies per unit of output magnitude: |err| <= max_abs *
-    max(1, |ref|).  Mean-abs is bounded absolutely."""
+
+def _excess(err, bound):
+    k = int(np.argmax(err - bound))
+    return f"max excess {np.max(err - bound):.3e} at flat index {k} (err {err.flat[k]:.3e}, bound {bound.flat[k]:.3e})"
+
+
+def check_f32(o, ref, b: Bound, lse=None, ref_lse=None):
+    """fp32 output: every element within the derived bound, the LSE within its bound."""
     assert np.all(np.isfinite(o))
     err = np.abs(o - ref)
-    excess = err - max_abs * np.maximum(1.0, np.abs(ref))
-    assert excess.max() <= 0, f"max-abs {err.max():.3e} (largest excess {excess.max():.3e})"
-    assert err.mean() <= mean_abs, f"mean-abs {err.mean():.3e}"
+    bound = b.f32(ref)
+    assert np.all(err <= bound), _excess(err, bound)
     if lse is not None:
         le = np.abs(lse - ref_lse)
-        assert le.max() <= lse_abs, f"lse max-abs {le.max():.3e}"
-    return err.max(), err.mean()
+        lb = b.lse(ref_lse)
+        assert np.all(le <= lb), "lse: " + _excess(le, lb)
+    return err
 
 
-def check_bf16(o, ref, max_abs=1e-2, mean_abs=1e-3):
-    """bf16 output: the fp32 tolerance plus half a bf16 ulp of rounding (2^-8 relative)."""
+def check_bf16(o, ref, b: Bound):
+    """bf16 output: the fp32 bound plus half a bf16 ulp of output rounding."""
     assert np.all(np.isfinite(o))
     err = np.abs(o - ref)
-    bound = max_abs * np.maximum(1.0, np.abs(ref)) + np.abs(ref) * 2.0 ** -8
-    assert np.all(err <= bound), f"max excess {np.max(err - bound):.3e}"
-    assert err.mean() <= mean_abs + np.mean(np.abs(ref)) * 2.0 ** -9, f"mean-abs {err.mean():.3e}"
+    bound = b.bf16(ref)
+    assert np.all(err <= bound), _excess(err, bound)
+    return err
+
+
+def check_literal(o, ref, max_abs=1e-2, mean_abs=1e-3):
+    """The stated gate, read literally on outputs bounded by 1 (|V| <= 1):
+    raw max-abs and mean-abs errors, element by element."""
+    assert np.all(np.isfinite(o))
+    assert np.max(np.abs(ref)) <= 1.0
+    err = np.abs(o - ref)
+    assert err.max() <= max_abs, f"max-abs {err.max():.3e}"
+    assert err.mean() <= mean_abs, f"mean-abs {err.mean():.3e}"
+    return err.max(), err.mean()
 
 
 def check_relative(o, ref, rel_fro=5e-3):
@@ -85,3 +108,19 @@ def check_relative(o, ref, rel_fro=5e-3):
     r = np.linalg.norm(o - ref) / np.linalg.norm(ref)
     assert r <= rel_fro, f"relative Frobenius error {r:.3e}"
     return r
+
+
+def check_f1(o, ref, b: Bound, out_bf16=False):
+    """Literal N(0,1)/sqrt(d) inputs (outputs ~1e-3): the worst-case bound,
+    the statistical (Hoeffding) bound per element, and the relative Frobenius
+    error.  Returns the errors normalised by rms(O), max and mean.  With a
+    bf16 output both bounds carry its rounding (half an ulp)."""
+    (check_bf16 if out_bf16 else check_f32)(o, ref, b)
+    err = np.abs(o - ref)
+    hb = b.hoeffding(ref)
+    if out_bf16:
+        hb = hb + U8 * (np.abs(ref) + hb)
+    assert np.all(err <= hb), "hoeffding: " + _excess(err, hb)
+    check_relative(o, ref)
+    rms = float(np.sqrt(np.mean(ref ** 2)))
+    return float(err.max() / rms), float(err.mean() / rms)

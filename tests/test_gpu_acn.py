@@ -1,7 +1,8 @@
 """GPU parity of the bidirectional in-chunk option and of the chunk-granular
 acn window (paper, Sec. 3 and the staircase mask of Eq. (4)) against the
 oracle, whose readings are pinned to the literal mask in
-test_oracle_acn_pins.py.  Tolerances as in test_gpu_parity.py."""
+test_oracle_acn_pins.py.  Tolerances: the derived per-element bounds of
+tests/_bounds.py, as in test_gpu_parity.py."""
 import numpy as np
 import pytest
 import torch
@@ -9,7 +10,8 @@ import torch
 import oracle
 import paper_2606_19849_amd as vico
 from synth import make_chunk_inputs, ragged_chunk_lengths, stream_chunk, stream_sink
-from tests._gpu import DeviceChunk, check_bf16, check_f32, dev, oracle_result
+from tests._bounds import chunk_bound
+from tests._gpu import DeviceChunk, check_bf16, check_f32, dev, oracle_and_bound
 from tests.test_gpu_parity import SMALL
 
 pytestmark = pytest.mark.gpu
@@ -20,16 +22,19 @@ BIDIR = vico.VICO_ATTN_BIDIRECTIONAL
 @pytest.mark.parametrize("splits", [0, 1, 3, -1])
 def test_bidirectional_small_f2_fp32(name, splits):
     inp = make_chunk_inputs(SMALL[name], seed=301, family="F2")
-    o, lse = DeviceChunk(inp).attention(torch.float32, num_splits=splits, flags=BIDIR)
-    ref, ref_lse = oracle_result(inp, bidirectional=True)
-    check_f32(o, ref, lse, ref_lse)
+    dc = DeviceChunk(inp)
+    o, lse = dc.attention(torch.float32, num_splits=splits, flags=BIDIR)
+    ref, ref_lse, b = oracle_and_bound(inp, bidirectional=True, parts=dc.parts)
+    check_f32(o, ref, b, lse, ref_lse)
 
 
 @pytest.mark.parametrize("name", ["tiny", "gqa7_ragged", "balanced_many_parts"])
 def test_bidirectional_bf16(name):
     inp = make_chunk_inputs(SMALL[name], seed=302, family="F2")
-    o, _ = DeviceChunk(inp).attention(torch.bfloat16, flags=BIDIR)
-    check_bf16(o, oracle_result(inp, bidirectional=True)[0])
+    dc = DeviceChunk(inp)
+    o, _ = dc.attention(torch.bfloat16, flags=BIDIR)
+    ref, _, b = oracle_and_bound(inp, bidirectional=True, parts=dc.parts)
+    check_bf16(o, ref, b)
 
 
 @pytest.mark.parametrize("cfg", ["7b_wrap", "3b_wrap"])
@@ -40,13 +45,14 @@ def test_bidirectional_full_size_sampled_rows(cfg):
     from synth import CONFIGS
     sh = CONFIGS[cfg]
     inp = make_chunk_inputs(sh, seed=5, family="F2")
-    o, lse = DeviceChunk(inp).attention(torch.bfloat16, flags=BIDIR)
+    dc = DeviceChunk(inp)
+    o, lse = dc.attention(torch.bfloat16, flags=BIDIR)
     rng = np.random.default_rng(3)
     rows = np.unique(np.concatenate([rng.choice(sh.chunk_len, 24, replace=False),
                                      [0, 255, 256, sh.chunk_len - 1]]))
-    ref, ref_lse = oracle_result(inp, rows=rows, bidirectional=True)
-    check_bf16(o[rows], ref)
-    assert np.max(np.abs(lse[:, rows] - ref_lse)) <= 1e-3
+    ref, ref_lse, b = oracle_and_bound(inp, rows=rows, bidirectional=True, parts=dc.parts)
+    check_bf16(o[rows], ref, b)
+    assert np.all(np.abs(lse[:, rows] - ref_lse) <= b.lse(ref_lse))
 
 
 @pytest.mark.parametrize("flags", [0, BIDIR])
@@ -82,10 +88,13 @@ def test_acn_window_stream(flags):
         l = lse[:, torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
         hk = np.concatenate(hk_all) if hk_all else np.zeros((0, Hkv, D))
         hv = np.concatenate(hv_all) if hv_all else np.zeros((0, Hkv, D))
-        ref, ref_lse = oracle.chunk_prefill_attention(
-            oracle.bf16_bits_to_f64(qb), oracle.bf16_bits_to_f64(kb), oracle.bf16_bits_to_f64(vb),
-            sk64, sv64, hk, hv, H, W, rows=rows, bidirectional=bool(flags & BIDIR))
-        check_f32(o, ref, l, ref_lse)
+        x = dict(q=oracle.bf16_bits_to_f64(qb), k_chunk=oracle.bf16_bits_to_f64(kb),
+                 v_chunk=oracle.bf16_bits_to_f64(vb), sink_k=sk64, sink_v=sv64, hist_k=hk, hist_v=hv,
+                 hist_len=H, window=W)
+        ref, ref_lse = oracle.chunk_prefill_attention(**x, rows=rows, bidirectional=bool(flags & BIDIR))
+        parts = vico.vico_attn_plan(c, S, R, H, W, Hq, Hkv, D, 0, flags)[0]
+        b = chunk_bound(x, rows=rows, bidirectional=bool(flags & BIDIR), parts=parts)
+        check_f32(o, ref, b, l, ref_lse)
         hk_all.append(oracle.bf16_bits_to_f64(kb))
         hv_all.append(oracle.bf16_bits_to_f64(vb))
         if len(hk_all) > acn + 1:

@@ -13,9 +13,9 @@ Bounds used here, derived from the arithmetic:
     GPU's selection.  Against the fp64 scores, the selection must equal the
     oracle's wherever the k-th and (k+1)-th scores are further apart than
     twice the cosine bound, and otherwise stay within that bound of it.
-  * gathered attention: as for the chunk prefill (bf16 probabilities):
-    |err| <= 1e-2 * max(1, |ref|), mean <= 1e-3 on the O(1) family, LSE
-    within 1e-3.
+  * gathered attention: the derived per-element bounds of tests/_bounds.py
+    (bf16 probabilities, fp32 logits and sums, the log-sum-exp merge of the
+    key-range parts), output and LSE, as for the chunk prefill.
 """
 from __future__ import annotations
 
@@ -29,7 +29,8 @@ import torch
 import oracle
 import paper_2606_19849_amd as vico
 from synth import CONFIGS, QUERY_CONFIGS, QueryShape, make_chunk_inputs, make_query_inputs, make_tokens
-from tests._gpu import bits_of, check_bf16, check_f32, dev
+from tests._bounds import Bound, chunk_bound, gather_bound
+from tests._gpu import check_bf16, check_f1, check_f32, dev
 from tests._util import ring_from_inputs, to_f64
 
 pytestmark = pytest.mark.gpu
@@ -194,12 +195,24 @@ class DeviceQuery:
         torch.cuda.synchronize()
         return out.float().cpu().numpy().astype(np.float64), lse.cpu().numpy().astype(np.float64), parts
 
-    def reference(self, seg_start, seg_len, q_rows=None, heads=None):
+    def reference(self, seg_start, seg_len, q_rows=None, heads=None, scale=None, parts=1, sigma=False):
+        """Oracle output, LSE and the derived bound; the oracle sees only the
+        store rows the segments name (a compacted copy, same order)."""
         qi = self.qi
         q = f64(qi.q) if q_rows is None else f64(qi.q)[-q_rows:]
         k, v = self.store_np
-        return oracle.gather_attention(q, f64(qi.tail_k), f64(qi.tail_v), f64(qi.sink_k), f64(qi.sink_v),
-                                       f64(k), f64(v), seg_start, seg_len, heads=heads)
+        seg_start = np.asarray(seg_start, np.int64)
+        seg_len = np.asarray(seg_len, np.int64)
+        d = qi.shape.head_dim
+        Hkv = qi.shape.num_kv_heads
+        ck = f64(np.concatenate([k[a:a + n] for a, n in zip(seg_start, seg_len)] or [k[:0]]))
+        cv = f64(np.concatenate([v[a:a + n] for a, n in zip(seg_start, seg_len)] or [v[:0]]))
+        cs = np.concatenate([[0], np.cumsum(seg_len)[:-1]]).astype(np.int64) if len(seg_len) else seg_start
+        args = (q, f64(qi.tail_k), f64(qi.tail_v), f64(qi.sink_k).reshape(-1, Hkv, d),
+                f64(qi.sink_v).reshape(-1, Hkv, d), ck.reshape(-1, Hkv, d), cv.reshape(-1, Hkv, d), cs, seg_len)
+        ro, rl = oracle.gather_attention(*args, heads=heads, scale=scale)
+        b = gather_bound(*args, heads=heads, scale=scale, parts=parts, sigma=sigma)
+        return ro, rl, b
 
 
 SMALL_Q = ["q_tiny", "q_small", "q_gqa7"]
@@ -213,8 +226,8 @@ def test_gather_attention_parity(name, splits):
     st, ln = oracle.chunk_segments(sel, qi.chunk_start, qi.chunk_len)
     d = DeviceQuery(qi)
     o, l, parts = d.attend(st, ln, num_splits=splits)
-    ro, rl = d.reference(st, ln)
-    check_f32(o, ro, l, rl)
+    ro, rl, b = d.reference(st, ln, parts=parts)
+    check_f32(o, ro, b, l, rl)
     if splits:
         assert parts == splits
 
@@ -225,8 +238,9 @@ def test_gather_attention_bf16_out(name):
     sel = oracle.select_chunks(np.random.default_rng(2).uniform(size=qi.shape.num_chunks), qi.shape.top_k)
     st, ln = oracle.chunk_segments(sel, qi.chunk_start, qi.chunk_len)
     d = DeviceQuery(qi)
-    o, _, _ = d.attend(st, ln, out_dtype=torch.bfloat16)
-    check_bf16(o, d.reference(st, ln)[0])
+    o, _, parts = d.attend(st, ln, out_dtype=torch.bfloat16)
+    ro, _, b = d.reference(st, ln, parts=parts)
+    check_bf16(o, ro, b)
 
 
 @pytest.mark.parametrize("splits", [0, 4])
@@ -235,9 +249,9 @@ def test_decode_step(splits):
     qi = make_query_inputs(QUERY_CONFIGS["q_gqa7"], seed=13, family="F2")
     st, ln = oracle.chunk_segments(np.array([0, 5, 6, 20]), qi.chunk_start, qi.chunk_len)
     d = DeviceQuery(qi)
-    o, l, _ = d.attend(st, ln, q_rows=1, num_splits=splits)
-    ro, rl = d.reference(st, ln, q_rows=1)
-    check_f32(o, ro, l, rl)
+    o, l, parts = d.attend(st, ln, q_rows=1, num_splits=splits)
+    ro, rl, b = d.reference(st, ln, q_rows=1, parts=parts)
+    check_f32(o, ro, b, l, rl)
 
 
 def test_decode_step_replays_as_a_graph():
@@ -268,8 +282,8 @@ def test_decode_step_replays_as_a_graph():
         step(i)
         torch.cuda.synchronize()
         eager.append((out.clone(), lse.clone()))
-    ro, rl = d.reference(*tables[0], q_rows=1)
-    check_f32(eager[0][0].cpu().numpy().astype(np.float64), ro, eager[0][1].cpu().numpy().astype(np.float64), rl)
+    ro, rl, b = d.reference(*tables[0], q_rows=1, parts=parts)
+    check_f32(eager[0][0].cpu().numpy().astype(np.float64), ro, b, eager[0][1].cpu().numpy().astype(np.float64), rl)
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -311,18 +325,16 @@ def test_gather_explicit_softmax_scale(scale):
                           torch.from_numpy(ln.astype(np.int32)).cuda(), out, lse=lse, workspace=ws,
                           keys_hint=hint, softmax_scale=scale)
     torch.cuda.synchronize()
-    k, v = d.store_np
-    ro, rl = oracle.gather_attention(f64(qi.q)[-Lq:], f64(qi.tail_k), f64(qi.tail_v), f64(qi.sink_k),
-                                     f64(qi.sink_v), f64(k), f64(v), st, ln, scale=scale)
-    check_f32(out.cpu().numpy().astype(np.float64), ro, lse.cpu().numpy().astype(np.float64), rl)
+    ro, rl, b = d.reference(st, ln, q_rows=Lq, scale=scale, parts=parts)
+    check_f32(out.cpu().numpy().astype(np.float64), ro, b, lse.cpu().numpy().astype(np.float64), rl)
 
 
 def test_no_segments_attends_sink_and_tail():
     qi = make_query_inputs(QUERY_CONFIGS["q_small"], seed=14, family="F2")
     d = DeviceQuery(qi)
-    o, l, _ = d.attend([], [])
-    ro, rl = d.reference([], [])
-    check_f32(o, ro, l, rl)
+    o, l, parts = d.attend([], [])
+    ro, rl, b = d.reference([], [], parts=parts)
+    check_f32(o, ro, b, l, rl)
 
 
 def test_segments_are_clipped_to_the_store():
@@ -336,9 +348,9 @@ def test_segments_are_clipped_to_the_store():
     hi = np.clip(st + ln, 0, n)
     keep = hi > lo
     d = DeviceQuery(qi)
-    o, l, _ = d.attend(st, ln)
-    ro, rl = d.reference(lo[keep], (hi - lo)[keep])
-    check_f32(o, ro, l, rl)
+    o, l, parts = d.attend(st, ln)
+    ro, rl, b = d.reference(lo[keep], (hi - lo)[keep], parts=parts)
+    check_f32(o, ro, b, l, rl)
 
 
 def test_many_tiny_segments():
@@ -350,9 +362,9 @@ def test_many_tiny_segments():
     ln = rng.integers(0, 3, 1500).astype(np.int64)
     lo, hi = np.clip(st, 0, qi.store_len), np.clip(st + ln, 0, qi.store_len)
     d = DeviceQuery(qi)
-    o, l, _ = d.attend(st, ln, num_splits=5)
-    ro, rl = d.reference(lo, np.maximum(hi - lo, 0))
-    check_f32(o, ro, l, rl)
+    o, l, parts = d.attend(st, ln, num_splits=5)
+    ro, rl, b = d.reference(lo, np.maximum(hi - lo, 0), parts=parts)
+    check_f32(o, ro, b, l, rl)
 
 
 def test_d64_and_mha():
@@ -361,8 +373,9 @@ def test_d64_and_mha():
     sel = oracle.select_chunks(np.random.default_rng(5).uniform(size=sh.num_chunks), sh.top_k)
     st, ln = oracle.chunk_segments(sel, qi.chunk_start, qi.chunk_len)
     d = DeviceQuery(qi)
-    o, l, _ = d.attend(st, ln, num_splits=2)
-    check_f32(o, *d.reference(st, ln)[:1], l, d.reference(st, ln)[1])
+    o, l, parts = d.attend(st, ln, num_splits=2)
+    ro, rl, b = d.reference(st, ln, parts=parts)
+    check_f32(o, ro, b, l, rl)
 
 
 def test_long_query_spans_two_row_tiles():
@@ -373,8 +386,9 @@ def test_long_query_spans_two_row_tiles():
     st, ln = oracle.chunk_segments(sel, qi.chunk_start, qi.chunk_len)
     d = DeviceQuery(qi)
     for splits in (0, 3):
-        o, l, _ = d.attend(st, ln, num_splits=splits)
-        check_f32(o, *d.reference(st, ln)[:1], l, d.reference(st, ln)[1])
+        o, l, parts = d.attend(st, ln, num_splits=splits)
+        ro, rl, b = d.reference(st, ln, parts=parts)
+        check_f32(o, ro, b, l, rl)
 
 
 def test_gather_over_ring_window_equals_chunk_prefill():
@@ -394,8 +408,12 @@ def test_gather_over_ring_window_equals_chunk_prefill():
                           torch.tensor(st, dtype=torch.int64, device="cuda"),
                           torch.tensor(ln, dtype=torch.int32, device="cuda"), out, lse=lse, keys_hint=wv)
     torch.cuda.synchronize()
-    ro, rl = oracle.chunk_prefill_attention(**to_f64(inp))
-    check_f32(out.cpu().numpy().astype(np.float64), ro, lse.cpu().numpy().astype(np.float64), rl)
+    parts = vico.vico_gather_plan(sh.chunk_len, sh.chunk_len, sh.sink_len, sh.ring_slots, 2, wv, sh.num_q_heads,
+                                  sh.num_kv_heads, sh.head_dim)[0]
+    x = to_f64(inp)
+    ro, rl = oracle.chunk_prefill_attention(**x)
+    check_f32(out.cpu().numpy().astype(np.float64), ro, chunk_bound(x, parts=parts),
+              lse.cpu().numpy().astype(np.float64), rl)
 
 
 # ---------------------------------------------------------------- whole query path at full size
@@ -451,8 +469,8 @@ def test_query_path_full_size(name):
     st, ln = oracle.chunk_segments(sel, qi.chunk_start, qi.chunk_len)
     assert np.array_equal(ss.cpu().numpy(), st) and np.array_equal(sl.cpu().numpy(), ln)
     # stage 4: attention over the selected chunks, every row and head
-    ro, rl = d.reference(st, ln)
-    check_f32(out.cpu().numpy().astype(np.float64), ro, lse.cpu().numpy().astype(np.float64), rl)
+    ro, rl, b = d.reference(st, ln, parts=parts)
+    check_f32(out.cpu().numpy().astype(np.float64), ro, b, lse.cpu().numpy().astype(np.float64), rl)
 
 
 def test_store_at_the_32bit_offset_limit():
@@ -490,9 +508,63 @@ def test_store_at_the_32bit_offset_limit():
     sv64, tv64 = sv.double().numpy()[:, 0], tv.double().numpy()[:, 0]
     o = out.cpu().double().numpy()
     l = lse.cpu().double().numpy()
+    seg_abs = float(marks(slots).sum()) * cvec.double().abs().numpy()
     for i in range(Lq):
         vis_tail = T - Lq + i + 1
         n = S + hint + vis_tail
         mean = (sv64.sum(0) + seg_sum + tv64[:vis_tail].sum(0)) / n
-        assert np.max(np.abs(o[i] - mean[None, :])) <= 1e-4
-        assert np.max(np.abs(l[:, i] - np.log(n))) <= 1e-4
+        # every logit is exactly 0, so every probability is exactly 1: only
+        # the fp32 sums and the merge round (the derived bound with no logit error)
+        A = (np.abs(sv64).sum(0) + seg_abs + np.abs(tv64[:vis_tail]).sum(0)) / n
+        b = Bound(A[None, None, :], np.zeros((1, 1)), np.zeros((1, 1)), n, parts)
+        assert np.all(np.abs(o[i] - mean[None, :]) <= b.f32(mean[None, None, :])[0])
+        assert np.all(np.abs(l[:, i] - np.log(n)) <= b.lse(np.log(n)))
+
+
+@pytest.mark.parametrize("family,query_seed", [("F1", 0), ("F1", 5), ("F2", 0)])
+def test_decode_step_full_size(family, query_seed):
+    """One decode step at full size, as timed: 7B heads (28 query, 4 KV,
+    d 128), a query row over sink 64 + the 32 chunks retrieved from a
+    256-chunk store (336 MB of K/V) + a 64-token tail, with the key-range
+    split the planner picks for it; retrieval on the device, bf16 output.
+    Every head's output element and LSE against the derived bound (for the
+    N(0,1)/sqrt(d) family also the statistical one)."""
+    base = dataclasses.replace(QUERY_CONFIGS["q_7b"], tail_len=64)
+    qi = make_query_inputs(base, seed=0, family=family, query_seed=query_seed)
+    sh = qi.shape
+    d = DeviceQuery(qi)
+    qf = torch.empty(sh.feat_dim, dtype=torch.float32, device="cuda")
+    scores = torch.empty(sh.num_chunks, dtype=torch.float32, device="cuda")
+    oc = torch.empty(sh.top_k, dtype=torch.int32, device="cuda")
+    os_ = torch.empty(sh.top_k, dtype=torch.float32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    ss = torch.empty(sh.top_k, dtype=torch.int64, device="cuda")
+    sl = torch.empty(sh.top_k, dtype=torch.int32, device="cuda")
+    vico.vico_token_mean(dev(qi.query_x), qf)
+    vico.vico_chunk_scores(qf, torch.from_numpy(qi.chunk_feat).cuda(), scores)
+    vico.vico_topk_chunks(scores, sh.top_k, oc, os_, cnt, chunk_start=torch.from_numpy(qi.chunk_start).cuda(),
+                          chunk_len=torch.from_numpy(qi.chunk_len.astype(np.int32)).cuda(), seg_start=ss,
+                          seg_len=sl)
+    hint = sh.top_k * (sh.chunk_lo + sh.chunk_hi) // 2
+    parts, wb = vico.vico_gather_plan(1, sh.tail_len, sh.sink_len, qi.store_len, sh.top_k, hint,
+                                      sh.num_q_heads, sh.num_kv_heads, sh.head_dim)
+    assert parts > 1                  # the split and the merge are part of the step
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+    out = torch.empty((1, sh.num_q_heads, sh.head_dim), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((sh.num_q_heads, 1), dtype=torch.float32, device="cuda")
+    vico.vico_gather_attn(d.q[-1:].contiguous(), d.tk, d.tv, d.sk, d.sv, d.gk, d.gv, ss, sl, out, lse=lse,
+                          workspace=ws, keys_hint=hint)
+    torch.cuda.synchronize()
+    n = int(cnt.item())
+    assert n == sh.top_k
+    st, ln = ss.cpu().numpy(), sl.cpu().numpy().astype(np.int64)
+    sel = oc.cpu().numpy()[:n]
+    assert np.array_equal(st, qi.chunk_start[sel]) and np.array_equal(ln, qi.chunk_len[sel])
+    o = out.float().cpu().numpy().astype(np.float64)
+    l = lse.cpu().numpy().astype(np.float64)
+    ro, rl, b = d.reference(st, ln, q_rows=1, parts=parts, sigma=family == "F1")
+    if family == "F1":
+        check_f1(o, ro, b, out_bf16=True)
+    else:
+        check_bf16(o, ro, b)
+    assert np.all(np.abs(l - rl) <= b.lse(rl))

@@ -1,7 +1,8 @@
 """Sustained streaming at the 3B layer shape: 64 chunks with ragged retained counts
 (uniform in [256, 1024]), sink 64, W = R = 8192; per chunk the library attends
 (history before the chunk, through the ring) and then appends.  Each chunk's
-sampled rows are checked against the oracle run on the linear history."""
+sampled rows are checked against the oracle run on the linear history, within
+the derived per-element bounds of tests/_bounds.py."""
 import numpy as np
 import pytest
 import torch
@@ -9,6 +10,7 @@ import torch
 import oracle
 import paper_2606_19849_amd as vico
 from synth import ragged_chunk_lengths, stream_chunk, stream_sink
+from tests._bounds import chunk_bound
 from tests._gpu import check_bf16, dev
 
 pytestmark = pytest.mark.gpu
@@ -46,11 +48,14 @@ def test_stream_of_ragged_chunks(window):
         l = lse[:, torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
         hk = np.concatenate(hist_k) if hist_k else np.zeros((0, Hkv, D))
         hv = np.concatenate(hist_v) if hist_v else np.zeros((0, Hkv, D))
-        ref, ref_lse = oracle.chunk_prefill_attention(
-            oracle.bf16_bits_to_f64(qb), oracle.bf16_bits_to_f64(kb), oracle.bf16_bits_to_f64(vb),
-            sk64, sv64, hk, hv, H, window, rows=rows)
-        check_bf16(o, ref)
-        assert np.max(np.abs(l - ref_lse)) <= 1e-3, f"chunk {t}"
+        x = dict(q=oracle.bf16_bits_to_f64(qb), k_chunk=oracle.bf16_bits_to_f64(kb),
+                 v_chunk=oracle.bf16_bits_to_f64(vb), sink_k=sk64, sink_v=sv64, hist_k=hk, hist_v=hv,
+                 hist_len=H, window=window)
+        ref, ref_lse = oracle.chunk_prefill_attention(**x, rows=rows)
+        parts = vico.vico_attn_plan(c, S, ring_slots, H, window, Hq, Hkv, D)[0]
+        b = chunk_bound(x, rows=rows, parts=parts)
+        check_bf16(o, ref, b)
+        assert np.all(np.abs(l - ref_lse) <= b.lse(ref_lse)), f"chunk {t}"
         hist_k.append(oracle.bf16_bits_to_f64(kb))
         hist_v.append(oracle.bf16_bits_to_f64(vb))
         if window >= 0 and sum(len(x) for x in hist_k) > 2 * W:      # keep the oracle's history short
