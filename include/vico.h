@@ -18,7 +18,8 @@
  * Conventions shared by every entry point
  *   - Tensors are dense, row-major, bfloat16 unless stated otherwise, in
  *     device memory owned by the caller.  The library never allocates or
- *     frees memory and keeps no state between calls.
+ *     frees memory and keeps no state between calls, except the fixed
+ *     device array of vico_gather_attn_noalloc (below).
  *   - Token-major layouts:  Q and O are [tokens][num_q_heads][head_dim];
  *     K/V (chunk, sink, ring) are [tokens][num_kv_heads][head_dim].
  *   - Ring slot p % ring_slots holds linear history token p.
@@ -48,7 +49,8 @@ typedef enum {
   VICO_ERR_CAPACITY = -3,     /* ring too small for the window or the chunk */
   VICO_ERR_MISALIGNED = -4,   /* pointer not 16-byte (lse_out: 4-byte) aligned */
   VICO_ERR_WORKSPACE = -5,    /* workspace missing or smaller than required */
-  VICO_ERR_HIP = -6           /* a HIP runtime call failed */
+  VICO_ERR_HIP = -6,          /* a HIP runtime call failed */
+  VICO_ERR_SCRATCH = -7       /* needs more than the fixed VICO_NOALLOC_SCRATCH_BYTES */
 } vico_status;
 
 enum { VICO_DTYPE_BF16 = 0, VICO_DTYPE_F32 = 1 };
@@ -282,6 +284,37 @@ int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const voi
 int vico_gather_plan(int32_t q_len, int32_t tail_len, int32_t sink_len, int32_t store_slots,
                      int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
                      int32_t head_dim, int32_t num_splits, int32_t* num_splits_out, int64_t* workspace_bytes_out);
+
+/*
+ * vico_gather_attn_noalloc -- vico_gather_attn for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, result and kernels as
+ * vico_gather_attn, without the workspace: the key-range partials go to a
+ * fixed device array of VICO_NOALLOC_SCRATCH_BYTES (64 MiB) inside the
+ * library.  The caller still owns q, K/V, the segment table, out and lse_out.
+ *
+ *   - A call whose plan (vico_gather_plan) needs more than
+ *     VICO_NOALLOC_SCRATCH_BYTES returns VICO_ERR_SCRATCH and enqueues
+ *     nothing.  The library's own split (num_splits = 0) needs at most
+ *     33.9 MB at head_dim 128 for any query length and head count, so only
+ *     an explicit num_splits can exceed it (a 7B decode step needs 0.9 MB).
+ *   - Each GPU gets its own copy of the array, created with the library's
+ *     code object on that GPU and held until the process ends.  Its address
+ *     is looked up on the first call made with that device current (before
+ *     capturing a graph, make one eager call on the device).
+ *   - Calls no hipMalloc, hipFree, hipMemset or copy; it only launches kernels.
+ *   - All calls on one GPU share its array: two calls that may run at the
+ *     same time on that GPU (different streams, no ordering between them)
+ *     race and give wrong results.  Calls ordered on one stream are fine;
+ *     every partial is written before it is read, so nothing is cleared.
+ */
+#define VICO_NOALLOC_SCRATCH_BYTES (64ll << 20)
+int vico_gather_attn_noalloc(const void* q, int32_t q_len, const void* tail_k, const void* tail_v, int32_t tail_len,
+                             const void* sink_k, const void* sink_v, int32_t sink_len, const void* store_k,
+                             const void* store_v, int32_t store_slots, const int64_t* seg_start,
+                             const int32_t* seg_len, int32_t num_segments, int64_t keys_hint, int32_t num_q_heads,
+                             int32_t num_kv_heads, int32_t head_dim, float softmax_scale, void* out,
+                             int32_t out_dtype, float* lse_out, int32_t num_splits, void* stream);
 
 /*
  * vico_temporal_drop -- chunk-level temporal token dropping (Sec. 3, "Token

@@ -17,6 +17,7 @@ from ._binding import (
     VICO_FULL_HISTORY,
     VICO_SPLIT_BALANCED,
     VICO_ATTN_BIDIRECTIONAL,
+    VICO_NOALLOC_SCRATCH_BYTES,
     VicoError,
     load_library,
     header_functions,
@@ -29,6 +30,7 @@ from ._binding import (
     vico_topk_chunks,
     vico_gather_plan,
     vico_gather_attn,
+    vico_gather_attn_noalloc,
     vico_acn_window,
     vico_temporal_drop,
 )
@@ -39,6 +41,7 @@ __all__ = [
     "VICO_FULL_HISTORY",
     "VICO_SPLIT_BALANCED",
     "VICO_ATTN_BIDIRECTIONAL",
+    "VICO_NOALLOC_SCRATCH_BYTES",
     "VicoError",
     "load_library",
     "header_functions",
@@ -51,6 +54,7 @@ __all__ = [
     "vico_topk_chunks",
     "vico_gather_plan",
     "vico_gather_attn",
+    "vico_gather_attn_noalloc",
     "vico_acn_window",
     "vico_temporal_drop",
 ]

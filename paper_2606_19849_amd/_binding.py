@@ -22,6 +22,7 @@ VICO_DTYPE_F32 = 1
 VICO_FULL_HISTORY = -1
 VICO_SPLIT_BALANCED = -1
 VICO_ATTN_BIDIRECTIONAL = 1
+VICO_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _i32, _i64, _f32, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
 
@@ -45,6 +46,8 @@ _SIGNATURES = {
                                 ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "vico_gather_attn": (_i32, [_vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _i64,
                                 _i32, _i32, _i32, _f32, _vp, _i32, _vp, _i32, _vp, _i64, _vp]),
+    "vico_gather_attn_noalloc": (_i32, [_vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32, _vp, _vp, _i32,
+                                        _i64, _i32, _i32, _i32, _f32, _vp, _i32, _vp, _i32, _vp]),
     "vico_status_str": (ctypes.c_char_p, [_i32]),
     "vico_last_hip_error": (_i32, []),
 }
@@ -236,10 +239,9 @@ def vico_gather_plan(q_len, tail_len, sink_len, store_slots, num_segments, keys_
     return ns.value, wb.value
 
 
-def vico_gather_attn(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out, lse=None,
-                     workspace=None, keys_hint: int = 0, num_splits: int = 0, softmax_scale: float = 0.0,
-                     stream=None) -> None:
-    """Short-query attention over sink ++ store segments ++ causal tail (vico_gather_attn)."""
+def _gather_args(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out, lse, keys_hint,
+                 softmax_scale):
+    """Checked leading arguments shared by vico_gather_attn and its no-alloc variant."""
     for n, t in (("q", q), ("tail_k", tail_k), ("tail_v", tail_v), ("sink_k", sink_k), ("sink_v", sink_v),
                  ("store_k", store_k), ("store_v", store_v)):
         _dev_bf16(n, t)
@@ -258,13 +260,32 @@ def vico_gather_attn(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_st
     if lse is not None and not (lse.is_cuda and lse.dtype == torch.float32 and lse.is_contiguous()
                                 and tuple(lse.shape) == (Hq, Lq)):
         raise ValueError("lse: expected a contiguous float32 CUDA tensor of shape [num_q_heads, q_len]")
-    wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
     odt = VICO_DTYPE_F32 if out.dtype == torch.float32 else VICO_DTYPE_BF16
-    st = load_library().vico_gather_attn(
-        _ptr(q), Lq, _ptr(tail_k), _ptr(tail_v), T, _ptr(sink_k), _ptr(sink_v), S, _ptr(store_k), _ptr(store_v),
-        cap, _ptr(seg_start), _ptr(seg_len), n_segs, int(keys_hint), Hq, Hkv, D, float(softmax_scale), _ptr(out),
-        odt, _ptr(lse), int(num_splits), _ptr(workspace), wb, _stream(stream))
+    return (_ptr(q), Lq, _ptr(tail_k), _ptr(tail_v), T, _ptr(sink_k), _ptr(sink_v), S, _ptr(store_k),
+            _ptr(store_v), cap, _ptr(seg_start), _ptr(seg_len), n_segs, int(keys_hint), Hq, Hkv, D,
+            float(softmax_scale), _ptr(out), odt, _ptr(lse))
+
+
+def vico_gather_attn(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out, lse=None,
+                     workspace=None, keys_hint: int = 0, num_splits: int = 0, softmax_scale: float = 0.0,
+                     stream=None) -> None:
+    """Short-query attention over sink ++ store segments ++ causal tail (vico_gather_attn)."""
+    args = _gather_args(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out, lse,
+                        keys_hint, softmax_scale)
+    wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = load_library().vico_gather_attn(*args, int(num_splits), _ptr(workspace), wb, _stream(stream))
     _check(st, "vico_gather_attn")
+
+
+def vico_gather_attn_noalloc(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out,
+                             lse=None, keys_hint: int = 0, num_splits: int = 0, softmax_scale: float = 0.0,
+                             stream=None) -> None:
+    """vico_gather_attn with the library's fixed device array as workspace
+    (vico_gather_attn_noalloc); allocates nothing, here or in the library."""
+    args = _gather_args(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v, seg_start, seg_len, out, lse,
+                        keys_hint, softmax_scale)
+    st = load_library().vico_gather_attn_noalloc(*args, int(num_splits), _stream(stream))
+    _check(st, "vico_gather_attn_noalloc")
 
 
 def vico_temporal_drop(frames, tau: float, keep, out_index, out_count, sim=None, out_tokens=None, prev_frame=None,

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libvico.so")
-SOURCES = ["attn_fwd.hip", "attn_merge.hip", "attn_gather.hip", "retrieve.hip", "token_drop.hip", "kv_append.hip", "vico_api.hip"]
+SOURCES = ["attn_fwd.hip", "attn_merge.hip", "attn_gather.hip", "retrieve.hip", "token_drop.hip", "kv_append.hip", "vico_api.hip", "noalloc.hip"]
 BENCH_LIB = os.path.join(PKG, "libvico_bench.so")
 BENCH_SOURCES = ["mfma_peak.hip"]
 

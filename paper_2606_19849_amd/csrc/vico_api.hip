@@ -180,6 +180,8 @@ int hip_fail(hipError_t e) {
 
 }  // namespace
 
+int vico::record_hip_failure(hipError_t e) { return hip_fail(e); }
+
 extern "C" {
 
 const char* vico_status_str(int status) {
@@ -191,6 +193,7 @@ const char* vico_status_str(int status) {
     case VICO_ERR_MISALIGNED: return "pointer not 16-byte aligned";
     case VICO_ERR_WORKSPACE: return "workspace missing or too small";
     case VICO_ERR_HIP: return "HIP runtime error";
+    case VICO_ERR_SCRATCH: return "call needs more than the library's fixed scratch array";
     default: return "unknown status";
   }
 }
@@ -408,6 +411,21 @@ int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const voi
                      int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
                      int32_t head_dim, float softmax_scale, void* out, int32_t out_dtype, float* lse_out,
                      int32_t num_splits, void* workspace, int64_t workspace_bytes, void* stream) {
+  return vico::gather_attn_entry(q, q_len, tail_k, tail_v, tail_len, sink_k, sink_v, sink_len, store_k, store_v,
+                                 store_slots, seg_start, seg_len, num_segments, keys_hint, num_q_heads,
+                                 num_kv_heads, head_dim, softmax_scale, out, out_dtype, lse_out, num_splits,
+                                 workspace, workspace_bytes, stream, nullptr);
+}
+
+}  // extern "C"
+
+int vico::gather_attn_entry(const void* q, int32_t q_len, const void* tail_k, const void* tail_v, int32_t tail_len,
+                            const void* sink_k, const void* sink_v, int32_t sink_len, const void* store_k,
+                            const void* store_v, int32_t store_slots, const int64_t* seg_start,
+                            const int32_t* seg_len, int32_t num_segments, int64_t keys_hint, int32_t num_q_heads,
+                            int32_t num_kv_heads, int32_t head_dim, float softmax_scale, void* out,
+                            int32_t out_dtype, float* lse_out, int32_t num_splits, void* workspace,
+                            int64_t workspace_bytes, void* stream, WorkspaceSource source) {
   GatherShape sh;
   int st = check_gather_shape(q_len, tail_len, sink_len, store_slots, num_segments, keys_hint, num_q_heads,
                               num_kv_heads, head_dim, num_splits, &sh);
@@ -424,7 +442,6 @@ int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const voi
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return VICO_ERR_MISALIGNED;
   if (!aligned_to(seg_start, 8) || !aligned_to(seg_len, 4) || !aligned_to(lse_out, 4)) return VICO_ERR_MISALIGNED;
-  if (sh.ws_bytes > 0 && (!workspace || workspace_bytes < sh.ws_bytes)) return VICO_ERR_WORKSPACE;
   const int64_t ob = int64_t(q_len) * num_q_heads * head_dim * (out_dtype == VICO_DTYPE_F32 ? 4 : 2);
   const int64_t row = int64_t(num_kv_heads) * head_dim * 2;
   const int64_t lb = lse_out ? int64_t(num_q_heads) * q_len * 4 : 0;
@@ -436,6 +453,12 @@ int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const voi
     if (ins[i] && (overlaps(out, ob, ins[i], inb[i]) || overlaps(lse_out, lb, ins[i], inb[i])))
       return VICO_ERR_INVALID_ARG;
   if (overlaps(out, ob, lse_out, lb)) return VICO_ERR_INVALID_ARG;
+  // the library's own workspace is looked up only for a call known to be valid
+  if (source && sh.ws_bytes > 0) {
+    st = source(sh.ws_bytes, &workspace, &workspace_bytes);
+    if (st != VICO_OK) return st;
+  }
+  if (sh.ws_bytes > 0 && (!workspace || workspace_bytes < sh.ws_bytes)) return VICO_ERR_WORKSPACE;
 
   vico::GatherArgs a{};
   a.q = (const uint16_t*)q;
@@ -465,6 +488,8 @@ int vico_gather_attn(const void* q, int32_t q_len, const void* tail_k, const voi
   const hipError_t e = vico::launch_gather(a, (hipStream_t)stream);
   return e == hipSuccess ? VICO_OK : hip_fail(e);
 }
+
+extern "C" {
 
 int vico_temporal_drop(const void* frames, int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
                        int32_t feat_dim, float tau, const void* prev_frame, uint8_t* keep, float* sim,

@@ -98,6 +98,23 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
 hipError_t launch_temporal_drop(const DropArgs& a, hipStream_t stream);
+// Records e as the calling thread's last HIP error; returns VICO_ERR_HIP.
+int record_hip_failure(hipError_t e);
+
+// Supplies a workspace of at least `need` bytes (address and size), or
+// returns a negative vico_status.
+using WorkspaceSource = int (*)(int64_t need, void** workspace, int64_t* workspace_bytes);
+
+// Body of vico_gather_attn.  With `source` set, the workspace arguments are
+// ignored when a workspace is needed: source() supplies it, and is called
+// only after every other argument has been checked.
+int gather_attn_entry(const void* q, int32_t q_len, const void* tail_k, const void* tail_v, int32_t tail_len,
+                      const void* sink_k, const void* sink_v, int32_t sink_len, const void* store_k,
+                      const void* store_v, int32_t store_slots, const int64_t* seg_start, const int32_t* seg_len,
+                      int32_t num_segments, int64_t keys_hint, int32_t num_q_heads, int32_t num_kv_heads,
+                      int32_t head_dim, float softmax_scale, void* out, int32_t out_dtype, float* lse_out,
+                      int32_t num_splits, void* workspace, int64_t workspace_bytes, void* stream,
+                      WorkspaceSource source);
 hipError_t launch_token_mean(const uint16_t* x, int L, int dm, float* out, hipStream_t stream);
 hipError_t launch_chunk_scores(const float* qf, const float* cf, int N, int dm, float* scores, hipStream_t stream);
 hipError_t launch_topk(const float* scores, int N, int k, float min_score, const int64_t* chunk_start,

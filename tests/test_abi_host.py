@@ -16,7 +16,7 @@ MIS = 0x10008
 EXPECTED = {"vico_kv_append", "vico_chunk_prefill_attn", "vico_attn_plan", "vico_attn_workspace_bytes",
             "vico_status_str", "vico_last_hip_error", "vico_token_mean", "vico_chunk_scores", "vico_topk_chunks",
             "vico_gather_plan", "vico_gather_attn", "vico_chunk_prefill_attn_ex", "vico_attn_plan_ex",
-            "vico_acn_window", "vico_temporal_drop"}
+            "vico_acn_window", "vico_temporal_drop", "vico_gather_attn_noalloc"}
 
 
 def test_header_declares_the_expected_entry_points():
@@ -38,7 +38,7 @@ def test_single_hip_runtime_in_process():
 
 
 def test_status_strings():
-    for s in range(-6, 1):
+    for s in range(-7, 1):
         assert lib.vico_status_str(s) and lib.vico_status_str(s) != b"unknown status"
     assert lib.vico_status_str(-99) == b"unknown status"
     assert lib.vico_last_hip_error() == 0
@@ -252,6 +252,61 @@ def test_gather_rejects_bad_arguments(kw, status):
 
 def test_gather_zero_rows_is_a_no_op():
     assert _gather(Lq=0) == 0
+
+
+def _gather_noalloc(**kw):
+    a = dict(q=A, Lq=4, tk=A + 0x100000, tv=A + 0x200000, T=6, sk=A + 0x300000, sv=A + 0x400000, S=8,
+             gk=A + 0x500000, gv=A + 0x600000, cap=500, ss=A + 0x700000, sl=A + 0x701000, n=3, hint=100,
+             Hq=2, Hkv=1, D=64, scale=0.0, out=B, odt=1, lse=None, splits=0)
+    a.update(kw)
+    return lib.vico_gather_attn_noalloc(a["q"], a["Lq"], a["tk"], a["tv"], a["T"], a["sk"], a["sv"], a["S"],
+                                        a["gk"], a["gv"], a["cap"], a["ss"], a["sl"], a["n"], a["hint"], a["Hq"],
+                                        a["Hkv"], a["D"], a["scale"], a["out"], a["odt"], a["lse"], a["splits"],
+                                        None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=3), -1),
+    (dict(D=80), -2),
+    (dict(q=None), -1),
+    (dict(q=MIS), -4),
+    (dict(out=A + 0x500000), -1),
+    (dict(n=2048, cap=1 << 20), -1),
+])
+def test_gather_noalloc_rejects_bad_arguments(kw, status):
+    """Argument checks are those of vico_gather_attn, made before the library's
+    array is looked up."""
+    assert _gather_noalloc(**kw) == status
+
+
+def test_gather_noalloc_rejects_work_beyond_its_array():
+    """A plan needing more partials than the fixed array holds fails before any
+    HIP call: 128 query rows at 28 heads, d 128, split 64 ways need 118 MB."""
+    kw = dict(Lq=128, T=128, S=64, cap=200000, n=32, hint=20480, Hq=28, Hkv=4, D=128, splits=64,
+              sk=A + (1 << 26), sv=A + (2 << 26), tk=A + (3 << 26), tv=A + (4 << 26), gk=A + (5 << 26),
+              gv=A + (7 << 26), ss=A + (9 << 26), sl=A + (10 << 26), out=A + (11 << 26))
+    wb = vico.vico_gather_plan(128, 128, 64, 200000, 32, 20480, 28, 4, 128, num_splits=64)[1]
+    assert wb > vico.VICO_NOALLOC_SCRATCH_BYTES
+    assert _gather_noalloc(**kw) == -7
+    assert lib.vico_status_str(-7) != b"unknown status"
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(28, 4, 128), (16, 2, 128), (64, 8, 128), (7, 1, 64)])
+def test_gather_noalloc_array_holds_every_default_plan(Hq, Hkv, D):
+    """With the library's own split every query length fits the array."""
+    for Lq in list(range(1, 300)) + list(range(300, 4097, 37)):
+        wb = vico.vico_gather_plan(Lq, Lq, 64, 200000, 32, 20480, Hq, Hkv, D)[1]
+        assert wb <= vico.VICO_NOALLOC_SCRATCH_BYTES, (Lq, wb)
+
+
+def test_gather_noalloc_zero_rows_is_a_no_op():
+    assert _gather_noalloc(Lq=0) == 0
+
+
+def test_noalloc_scratch_size_matches_the_header():
+    src = open(vico.load_library.__globals__["HEADER"]).read()
+    assert "#define VICO_NOALLOC_SCRATCH_BYTES (64ll << 20)" in src
+    assert vico.VICO_NOALLOC_SCRATCH_BYTES == 64 << 20
 
 
 def test_gather_plan_parts():
