@@ -65,16 +65,57 @@ def measured_traffic(kernel, workload):
     return float(fields["hbm_bytes_per_launch"])
 
 
-def hold_gpu(torch, stream, cycles=10_000_000):
-    """Queue a bounded spin (a few ms) ahead of a timed loop of short calls, so
-    that the host enqueues the calls faster than the GPU runs them: the events
-    around each call then bracket its kernels rather than the Python call
-    overhead that would otherwise pace an idle GPU."""
-    sleep = getattr(torch.cuda, "_sleep", None)
-    if sleep is None:       # without it the events stay host-paced (upper bounds on kernel time)
-        return
-    with torch.cuda.stream(stream):
-        sleep(cycles)
+class Busy:
+    """Matrix-core work on every CU (libvico_bench.so, register-only MFMA
+    chains) used to hold the GPU under load: ahead of a loop of short calls it
+    lets the host enqueue the calls faster than the GPU runs them, so the
+    events around each call bracket its kernels rather than Python call
+    overhead, and unlike an idle spin it keeps the engine clock where the
+    power manager holds it under load (after an idle period the clock takes
+    tens of milliseconds to climb back)."""
+
+    def __init__(self, torch):
+        import ctypes
+        from paper_2606_19849_amd.build import BENCH_LIB
+        lib = ctypes.CDLL(BENCH_LIB)
+        self.fn = lib.vico_bench_mfma_peak
+        self.fn.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+        self.fn.restype = ctypes.c_int32
+        self.torch = torch
+        self.groups = torch.cuda.get_device_properties(0).multi_processor_count
+        self.sink = torch.empty(self.groups * 8, dtype=torch.float32, device="cuda")
+        self.ms_per_iter = None
+
+    def launch(self, iters, stream):
+        if self.fn(self.groups, int(iters), self.sink.data_ptr(), stream.cuda_stream) != 0:
+            raise RuntimeError("vico_bench_mfma_peak failed")
+
+    def hold(self, stream, ms=4.0):
+        torch = self.torch
+        if self.ms_per_iter is None:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for _ in range(2):
+                a.record(stream)
+                self.launch(200, stream)
+                b.record(stream)
+                torch.cuda.synchronize()
+            self.ms_per_iter = a.elapsed_time(b) / 200
+        self.launch(max(1, ms / self.ms_per_iter), stream)
+
+
+def warm_up(torch, call, min_steps, seconds):
+    """Run `call(i)` for at least `min_steps` calls and `seconds` of wall time,
+    back to back, so the timed loop starts with the GPU at its loaded clock
+    (the power manager raises it over tens of milliseconds of work).  Returns
+    the number of calls made."""
+    i = 0
+    t0 = time.perf_counter()
+    while i < min_steps or time.perf_counter() - t0 < seconds:
+        call(i)
+        i += 1
+        if i % 64 == 0:
+            torch.cuda.synchronize()      # keep the queue short
+    return i
 
 
 def attn_flops(C, S, Wv, Hq, D, rows=None):
@@ -105,6 +146,18 @@ DESCR = {
 }
 
 
+def cpu_model():
+    """Host CPU model name (from /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(inp, n_rows, seed=0):
     """Time the fp64 oracle on `n_rows` rows (all heads) of the same chunk."""
     import oracle
@@ -122,6 +175,7 @@ def cpu_baseline(inp, n_rows, seed=0):
     dt = time.perf_counter() - t0
     fl = attn_flops(sh.chunk_len, sh.sink_len, sh.visible_window, sh.num_q_heads, sh.head_dim, rows)
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{n_rows} evenly spaced rows of the chunk x all {sh.num_q_heads} heads "
                       f"({fl / 1e9:.1f} GFLOP fp64) in {dt:.1f} s",
             "tokens_per_s": n_rows / dt}
@@ -159,7 +213,17 @@ def sustained_mfma_tflops(torch, stream, iters=2000, reps=5):
     return flops / (float(np.median(ms)) * 1e-3) / 1e12
 
 
+FLUSH_BYTES = 512 << 20      # > the 256 MB last-level cache + 8 x 4 MB L2
+
+
 def run_chunk_workload(args, torch, vico):
+    """Chunk prefill + append, timed in four variants: warm caches or flushed
+    (a 512 MiB write before every step evicts the L2s and the last-level
+    cache), and the wrapped ring phase of the workload (history = 5R + 777:
+    the window starts mid-tile and one key tile straddles the ring end) or the
+    aligned one (history = 5R: window start and ring end on tile bounds).  The
+    history advances by the chunk length every step.  The headline (`value`,
+    `roofline`) is the worst of the four."""
     from synth import make_chunk_inputs
     sh = workload_shape(args.workload)
     inp = make_chunk_inputs(sh, seed=0, family="F1")
@@ -173,21 +237,21 @@ def run_chunk_workload(args, torch, vico):
     vico.vico_kv_append(_dev(torch, inp.hist_k), _dev(torch, inp.hist_v), rk, rv, inp.hist_first)
     out = torch.empty((C, Hq, D), dtype=torch.bfloat16, device="cuda")
     lse = torch.empty((Hq, C), dtype=torch.float32, device="cuda")
-    H0 = sh.hist_len
     full = W < 0
-    n_total = args.warmup + args.steps
-    plans = []
-    for i in range(n_total):
-        H = H0 if full else H0 + i * C          # full-history control keeps its history fixed
-        plans.append((H,) + vico.vico_attn_plan(C, S, R, H, W, Hq, Hkv, D))
-    wb = max(p[2] for p in plans)
+    K = args.steps
+    # history of step i in each ring phase (the full-history control keeps its history fixed)
+    phases = {"wrapped": lambda i: sh.hist_len + i * C} if not full else {"fixed": lambda i: sh.hist_len}
+    if not full:
+        phases["aligned"] = lambda i: (sh.hist_len // R) * R + i * C
+        assert ((phases["aligned"](0) - min(W, phases["aligned"](0))) % R) % 64 == 0
+    n_plan = max(K, 4096)
+    wb = max(vico.vico_attn_plan(C, S, R, f(i), W, Hq, Hkv, D)[1] for f in phases.values() for i in (0, 1, 7, n_plan))
+    splits = vico.vico_attn_plan(C, S, R, phases[next(iter(phases))](0), W, Hq, Hkv, D)[0]
     ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
 
-    def step(i, events=None):
-        H = plans[i][0]
+    def step(H, events=None):
         if events:
             events[0].record(stream)
         vico.vico_chunk_prefill_attn(q, kc, vc, sk, sv, rk, rv, H, W, out, lse=lse, workspace=ws, stream=stream)
@@ -198,45 +262,77 @@ def run_chunk_workload(args, torch, vico):
         if events:
             events[2].record(stream)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for j in range(args.steps):
-        step(args.warmup + j, ev[j])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    attn_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
-    app_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
-    assert torch.isfinite(out.float()).all().item(), "non-finite attention output"
+    def flushed_step(H, j, events=None, fevents=None):
+        if fevents:
+            fevents[0].record(stream)
+        flush.fill_(j & 255)
+        if fevents:
+            fevents[1].record(stream)
+        step(H, events)
 
-    Wv = sh.visible_window
-    fl = attn_flops(C, S, Wv, Hq, D)
-    ms_step = elapsed * 1e3 / args.steps
-    achieved = fl / (attn_ms.mean() * 1e-3) / 1e12
+    fl = attn_flops(C, S, sh.visible_window, Hq, D)
+    variants = {}
+    n_warm = 0
+    for cache in ("warm", "flushed"):
+        for phase, H_of in phases.items():
+            ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(K)]
+            fev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(2)) for _ in range(K)]
+            # each variant is warmed up on its own steps right before it is timed: an idle
+            # GPU drops its clock, and it takes tens of milliseconds of work to climb back
+            if cache == "warm":
+                nw = warm_up(torch, lambda i: step(H_of(i)), args.warmup, args.warmup_seconds)
+            else:
+                nw = warm_up(torch, lambda i: flushed_step(H_of(i), i), args.warmup, args.warmup_seconds)
+            n_warm = max(n_warm, nw)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for j in range(K):
+                if cache == "flushed":
+                    flushed_step(H_of(nw + j), j, ev[j], fev[j])
+                else:
+                    step(H_of(nw + j), ev[j])
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            attn_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+            app_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+            flush_s = sum(a.elapsed_time(b) for a, b in fev) * 1e-3 if cache == "flushed" else 0.0
+            step_s = (wall - flush_s) / K        # wall clock per step, flush kernels excluded
+            variants[f"{cache}_{phase}"] = {
+                "attn_us_mean": round(float(attn_ms.mean()) * 1e3, 2),
+                "attn_us_median": round(float(np.median(attn_ms)) * 1e3, 2),
+                "append_us_mean": round(float(app_ms.mean()) * 1e3, 2) if not full else None,
+                "step_ms_wall": round(step_s * 1e3, 4),
+                "attn_tflops": round(fl / (attn_ms.mean() * 1e-3) / 1e12, 2),
+                "step_tflops": round(fl / step_s / 1e12, 2),
+            }
+    worst = min(variants, key=lambda k: variants[k]["step_tflops"])
+    worst_attn = min(variants, key=lambda k: variants[k]["attn_tflops"])
+    achieved = variants[worst_attn]["attn_tflops"]
+    w = variants[worst]
     app_bytes = 2 * 2 * C * Hkv * D * 2          # K and V, read + write
     res = {
         "metric": "chunk-prefill attention TFLOP/s (% bf16 MFMA peak) + visual tokens/s per layer",
-        "value": round(fl * args.steps / elapsed / 1e12, 2),
+        "value": w["step_tflops"],
         "unit": "TFLOP/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "n_gpus": 1, "steps": K, "warmup": n_warm,
+        "ms_per_step": w["step_ms_wall"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": DESCR[args.workload], "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D,
-                   "sink": S, "window": W, "ring_slots": R, "chunk": C, "hist_start": H0,
-                   "splits": plans[-1][1], "out_dtype": "bf16", "inputs": "N(0,1)/sqrt(d) bf16, seed 0"},
-        "pct_peak": round(100 * fl * args.steps / elapsed / 1e12 / PEAK_BF16_TFLOPS, 2),
-        "visual_tokens_per_s": round(C * args.steps / elapsed, 1),
-        "attn_ms_mean": round(float(attn_ms.mean()), 4),
-        "attn_ms_median": round(float(np.median(attn_ms)), 4),
-        "append_ms_mean": round(float(app_ms.mean()), 4) if not full else None,
-        "append_GBps": round(app_bytes / (app_ms.mean() * 1e-3) / 1e9, 1) if not full else None,
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                   "sink": S, "window": W, "ring_slots": R, "chunk": C, "hist_start": sh.hist_len,
+                   "splits": splits, "out_dtype": "bf16", "inputs": "N(0,1)/sqrt(d) bf16, seed 0"},
+        "headline_variant": worst,
+        "pct_peak": round(100 * w["step_tflops"] / PEAK_BF16_TFLOPS, 2),
+        "visual_tokens_per_s": round(C / (w["step_ms_wall"] * 1e-3), 1),
+        "attn_ms_mean": round(variants[worst_attn]["attn_us_mean"] * 1e-3, 4),
+        "append_GBps": round(app_bytes / (w["append_us_mean"] * 1e-6) / 1e9, 1) if not full else None,
+        "variants": variants,
+        "warmup_seconds": args.warmup_seconds,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": args.traffic_bytes if args.traffic_bytes is not None
                      else measured_traffic("attn_fwd_kernel<128>", args.workload),
-                     "kernel": "attn_fwd_kernel<128>",
+                     "kernel": "attn_fwd_kernel<128>", "variant": worst_attn,
                      "flops_per_launch": fl},
     }
     sustained = sustained_mfma_tflops(torch, stream)
@@ -245,6 +341,59 @@ def run_chunk_workload(args, torch, vico):
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_rows)
     return res
+
+
+def run_ramp_study(args, torch, vico):
+    """Chunk attention time against time since the GPU left an idle period:
+    the power manager lowers the engine clock when the GPU idles and raises it
+    again over tens of milliseconds of work, so a short timed loop that starts
+    right after an idle gap (a host synchronisation followed by slow host
+    work, or an idle spin kernel queued ahead of the loop) measures part of the
+    climb.  Prints per-call times of consecutive batches after (a) 1 s of
+    continuous work, (b) a 200 ms host sleep, (c) a 10 ms idle spin kernel."""
+    from synth import make_chunk_inputs
+    sh = workload_shape(args.workload)
+    inp = make_chunk_inputs(sh, seed=0, family="F1")
+    q, kc, vc = _dev(torch, inp.q), _dev(torch, inp.k_chunk), _dev(torch, inp.v_chunk)
+    sk, sv = _dev(torch, inp.sink_k), _dev(torch, inp.sink_v)
+    C, S, R, Hq, Hkv, D, W = (sh.chunk_len, sh.sink_len, sh.ring_slots, sh.num_q_heads, sh.num_kv_heads,
+                              sh.head_dim, sh.window)
+    rk = torch.zeros((R, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    rv = torch.zeros_like(rk)
+    vico.vico_kv_append(_dev(torch, inp.hist_k), _dev(torch, inp.hist_v), rk, rv, inp.hist_first)
+    out = torch.empty((C, Hq, D), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(vico.vico_attn_plan(C, S, R, sh.hist_len, W, Hq, Hkv, D)[1], 256), dtype=torch.uint8,
+                     device="cuda")
+    stream = torch.cuda.current_stream()
+    fl = attn_flops(C, S, sh.visible_window, Hq, D)
+    call = lambda: vico.vico_chunk_prefill_attn(q, kc, vc, sk, sv, rk, rv, sh.hist_len, W, out, workspace=ws,
+                                                stream=stream)
+
+    def batches(n_batches, per=4):
+        evs = []
+        for b in range(n_batches):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(per):
+                call()
+            e1.record(stream)
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        t = np.cumsum([a.elapsed_time(b) for a, b in evs])
+        return [(round(float(tt), 2), round(a.elapsed_time(b) / per * 1e3, 1)) for tt, (a, b) in zip(t, evs)]
+
+    warm_up(torch, lambda i: call(), 10, 1.0)
+    res = {"after_continuous_work_ms_us": batches(40)}
+    time.sleep(0.2)
+    res["after_200ms_host_sleep_ms_us"] = batches(40)
+    warm_up(torch, lambda i: call(), 10, 1.0)
+    torch.cuda._sleep(20_000_000)
+    res["after_10ms_idle_spin_ms_us"] = batches(40)
+    steady = np.median([x[1] for x in res["after_continuous_work_ms_us"]])
+    return {"metric": "chunk attention time after idle (clock ramp study)", "value": round(float(steady), 1),
+            "unit": "us per call, steady", "n_gpus": 1, "steps": 160, "warmup": None, "higher_is_better": False,
+            "config": {"workload": DESCR[args.workload]}, "flops_per_call": fl,
+            "series": "pairs (ms since the first batch began, us per call of that batch of 4)", **res}
 
 
 def run_stream_workload(args, torch, vico):
@@ -267,9 +416,15 @@ def run_stream_workload(args, torch, vico):
         outs = [torch.empty((int(c), Hq, D), dtype=torch.bfloat16, device="cuda") for c in counts]
         stream = torch.cuda.current_stream()
         lat = np.zeros((args.steps, len(counts)))
-        for rep in range(args.warmup + args.steps):
+        busy = Busy(torch)
+        t_warm = time.perf_counter()
+        rep, n_warm = 0, None
+        while n_warm is None or rep < n_warm + args.steps:
+            if n_warm is None and rep >= args.warmup and time.perf_counter() - t_warm >= args.warmup_seconds:
+                n_warm = rep
             ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
                    torch.cuda.Event(enable_timing=True)) for _ in counts]
+            busy.hold(stream, ms=6.0)
             for t, c in enumerate(counts):
                 q, k, v = chunks[t]
                 ev[t][0].record(stream)
@@ -279,8 +434,9 @@ def run_stream_workload(args, torch, vico):
                 vico.vico_kv_append(k, v, rk, rv, int(starts[t]), stream=stream)
                 ev[t][2].record(stream)
             torch.cuda.synchronize()
-            if rep >= args.warmup:
-                lat[rep - args.warmup] = [e[0].elapsed_time(e[2]) for e in ev]
+            if n_warm is not None:
+                lat[rep - n_warm] = [e[0].elapsed_time(e[2]) for e in ev]
+            rep += 1
         med = np.median(lat, axis=0)
         flops = np.array([attn_flops(int(c), S, min(int(starts[t]), W) if window >= 0 else int(starts[t]), Hq, D)
                           for t, c in enumerate(counts)])
@@ -300,7 +456,7 @@ def run_stream_workload(args, torch, vico):
     return {
         "metric": "chunk-prefill attention TFLOP/s (% bf16 MFMA peak) + visual tokens/s per layer",
         "value": b["tokens_per_s"], "unit": "visual tokens/s per layer",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm,
         "ms_per_step": round(sum(b["per_chunk_ms"]), 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
@@ -378,21 +534,21 @@ def run_query_workload(args, torch, vico):
         if events:
             events[2].record(stream)
 
-    for j in range(args.warmup):
-        step(j)
+    n_warm = warm_up(torch, step, args.warmup, args.warmup_seconds)
+    busy = Busy(torch)
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    hold_gpu(torch, stream)
+    busy.hold(stream)
     for j in range(args.steps):
-        step(args.warmup + j, ev[j])
+        step(n_warm + j, ev[j])
     torch.cuda.synchronize()
     host_paced = args.steps / (time.perf_counter() - t0)
     elapsed = ev[0][0].elapsed_time(ev[-1][2]) * 1e-3          # GPU span of the steps, fed ahead
     ret_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
     att_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
     Hq, Hkv, D, S, T = sh.num_q_heads, sh.num_kv_heads, sh.head_dim, sh.sink_len, sh.tail_len
-    G = np.array([gathered[(args.warmup + j) % n_q] for j in range(args.steps)], dtype=np.float64)
+    G = np.array([gathered[(n_warm + j) % n_q] for j in range(args.steps)], dtype=np.float64)
     keys = S + G + T
     kv_bytes = keys * Hkv * D * 2 * 2
     bytes_ = kv_bytes + Lq * Hq * D * 2 * 2 + Hq * Lq * 4            # + Q, O (bf16), LSE
@@ -406,7 +562,7 @@ def run_query_workload(args, torch, vico):
         "metric": ("decode-step attention per layer" if decode else
                    "query-side retrieval + gathered attention per layer (TTFT building block)"),
         "value": round(args.steps / elapsed, 1), "unit": "steps/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": DESCR[args.workload], "q_rows": Lq, "tail": T, "top_k": sh.top_k,
                    "stored_chunks": sh.num_chunks, "store_tokens": qi0.store_len, "parts": parts,
@@ -446,29 +602,31 @@ def run_drop_workload(args, torch, vico):
         vico.vico_temporal_drop(fr, tau, keep, idx, cnt, out_tokens=out, stream=stream)
         torch.cuda.synchronize()
         kept.append(int(cnt.item()))
-    for j in range(args.warmup):
-        vico.vico_temporal_drop(batches[j % n_batches], tau, keep, idx, cnt, out_tokens=out, stream=stream)
+    n_warm = warm_up(torch, lambda j: vico.vico_temporal_drop(batches[j % n_batches], tau, keep, idx, cnt,
+                                                              out_tokens=out, stream=stream),
+                     args.warmup, args.warmup_seconds)
+    busy = Busy(torch)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    hold_gpu(torch, stream)
+    busy.hold(stream)
     for j in range(args.steps):
         ev[j][0].record(stream)
-        vico.vico_temporal_drop(batches[(args.warmup + j) % n_batches], tau, keep, idx, cnt, out_tokens=out,
+        vico.vico_temporal_drop(batches[(n_warm + j) % n_batches], tau, keep, idx, cnt, out_tokens=out,
                                 stream=stream)
         ev[j][1].record(stream)
     torch.cuda.synchronize()
     host_paced = B * C * n_f * args.steps / (time.perf_counter() - t0)
     elapsed = ev[0][0].elapsed_time(ev[-1][1]) * 1e-3          # GPU span of the calls, fed ahead
     ms = np.array([a.elapsed_time(b) for a, b in ev])
-    n_keep = np.array([kept[(args.warmup + j) % n_batches] for j in range(args.steps)], dtype=np.float64)
+    n_keep = np.array([kept[(n_warm + j) % n_batches] for j in range(args.steps)], dtype=np.float64)
     in_bytes = B * C * n_f * dm * 2
     alg = in_bytes + n_keep * (dm * 2 + 4) + B * n_f
     gbs = float(np.mean(alg / (ms * 1e-3)) / 1e9)
     return {
         "metric": "temporal token dropping throughput (input tokens/s)",
         "value": round(B * C * n_f * args.steps / elapsed, 1), "unit": "tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": DESCR["drop"], "retention": round(float(n_keep.mean()) / (B * C * n_f), 4)},
         "call_us_mean": round(float(ms.mean()) * 1e3, 2),
@@ -492,12 +650,13 @@ def run_append_workload(args, torch, vico):
     rk = torch.zeros((R, Hkv, D), dtype=torch.bfloat16, device="cuda")
     rv = torch.zeros_like(rk)
     stream = torch.cuda.current_stream()
-    for i in range(args.warmup):
-        vico.vico_kv_append(k, v, rk, rv, 777 + i, stream=stream)
+    n_warm = warm_up(torch, lambda i: vico.vico_kv_append(k, v, rk, rv, 777 + i, stream=stream), args.warmup,
+                     args.warmup_seconds)
+    busy = Busy(torch)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    hold_gpu(torch, stream)
+    busy.hold(stream)
     for i in range(args.steps):
         ev[i][0].record(stream)
         vico.vico_kv_append(k, v, rk, rv, 777 + i * 1000, stream=stream)
@@ -510,7 +669,7 @@ def run_append_workload(args, torch, vico):
     gbs = nbytes / (ms.mean() * 1e-3) / 1e9
     return {
         "metric": "ring append HBM GB/s", "value": round(nbytes * args.steps / elapsed / 1e9, 1), "unit": "GB/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "ring append at capacity: 16384 tokens x 4 kv heads x d128, K and V, ring wraps",
                    "bytes_per_launch": nbytes},
@@ -528,9 +687,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup-seconds", type=float, default=1.0,
+                    help="warm-up also lasts at least this long, so timing starts at the loaded clock")
     ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append", "query", "decode",
                                                           "drop"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ramp", action="store_true",
+                    help="instead of the benchmark: chunk attention time against time since an idle period")
     ap.add_argument("--cpu-rows", type=int, default=2048)
     ap.add_argument("--traffic-bytes", type=float, default=None,
                     help="HBM bytes per attention launch from rocprofv3 FETCH_SIZE+WRITE_SIZE, if measured")
@@ -546,7 +709,9 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     vico.load_library()
-    if args.workload == "stream":
+    if args.ramp:
+        res = run_ramp_study(args, torch, vico)
+    elif args.workload == "stream":
         res = run_stream_workload(args, torch, vico)
     elif args.workload == "append":
         res = run_append_workload(args, torch, vico)
