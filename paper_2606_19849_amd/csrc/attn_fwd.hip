@@ -11,25 +11,9 @@
 //     rows of one query head (one key range when split).  Each wave owns 32
 //     rows for the whole key loop; every K/V tile brought into LDS serves all
 //     256 rows.
-//   * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: the K tile (from LDS) is the
-//     A operand, the wave's Q rows (held in VGPRs for the whole loop) the B
-//     operand.  In the accumulator layout lane l then holds 16 logits of
-//     query row l%32, and lanes l and l+32 together hold all 32 keys of the
-//     block, so the row max / row sum need a single v_permlane32_swap.
-//   * O^T = V^T P^T with the same MFMA: the S^T accumulator registers,
-//     rounded to bf16, are already the B operand (k index = key slot, keys
-//     of each 16-key group in the order the accumulator produces them); the
-//     A operand V^T is read from the row-major V tile with the gfx950
-//     transposing LDS read ds_read_b64_tr_b16 (each 16-lane group reads a
-//     4-key x 16-dim block and lane i receives dim i of the 4 keys).  O^T stays
-//     in the layout "lane = query row", so per-row rescale factors are
-//     lane-local.
-//   * Online softmax in fp32 with exp2 (v_exp_f32), scale*log2(e) folded into
-//     one FMA per logit.  Each half is exponentiated against the running max
-//     straight away; the max is only raised (and O rescaled, the half redone)
-//     when some lane's sum of probabilities exceeds 2^8, which bounds every
-//     probability by 2^8, or while a row has no max yet.  So no row-max
-//     reduction sits between the logits and the exponentials.
+//   * The tile body (S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_32x32x16_bf16,
+//     the exponentiate-first online softmax, two 32-key halves) is WaveTile
+//     of attn_common.h, shared with the gathered-query kernel.
 //   * K/V tiles: 64 keys, double-buffered in LDS; the next tile's loads
 //     are in flight while the current tile is multiplied.  Loads go through
 //     buffer resources (one per sink / ring / chunk tensor): a tile that lies
@@ -59,17 +43,10 @@ namespace {
 template <int D>
 __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a, int n_rt, int g) {
   constexpr int BN = kKeyTile;         // keys per tile
-  constexpr int RB = kRowBlocks;       // 32-row blocks per wave
   constexpr int BM = kBlockM;          // rows per work-group
-  constexpr int NKS = D / 16;          // k-steps of Q K^T
-  constexpr int NDB = D / 32;          // 32-dim blocks of O^T
-  // LDS tiles are dense rows of 2*D bytes (the direct loads below write each
-  // wave's 64 x 16 bytes contiguously), with 16-byte units permuted inside a
-  // row against bank conflicts; the LDS has 64 banks of 4 bytes:
-  //   K: unit u of row r sits at u ^ fk(r).  A K fragment read services 16
-  //      lanes = 16 consecutive rows at one unit; fk makes them distinct.
-  //   V: unit u of row r sits at u ^ fv(r).  A transposing read services 32
-  //      lanes = 4 consecutive rows x 4 units; fv spreads the rows apart.
+  static_assert(kRowBlocks == 1, "one 32-row block per wave (the shared tile body)");
+  // LDS tiles: dense rows of 2*D bytes (the direct loads below write each
+  // wave's 64 x 16 bytes contiguously), units swizzled as the tile body reads them
   constexpr int UPR = D / 8;           // 16-byte units per row
   constexpr int RBY = D * 2;           // bytes per LDS row
   constexpr int KT = BN * D;           // elements of one K (or V) tile
@@ -79,11 +56,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   constexpr int RPL = 1024 / RBY;            // rows per direct load
   constexpr int NBUF = kBuffers;
   static_assert(NLD * NW * 1024 == BN * RBY, "direct loads cover the tile");
-  static_assert(BM == NW * RB * 32, "work-group rows");
+  static_assert(BM == NW * 32, "work-group rows");
   static_assert(NBUF == 2 || NBUF == 3, "two or three LDS buffers");
   static_assert(BN % 64 == 0, "key tiles are whole 64-key sub-tiles");
-  auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
-  auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
 
   // NBUF K/V buffers: tile t lives in buffer t mod NBUF and is loaded NBUF-1
   // tiles ahead.  Separate arrays let the compiler see that reads of one
@@ -106,8 +81,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   const int wave = tid >> 6;
   const int l32 = lane & 31;
   const int hh = lane >> 5;
-
   const int C = a.C, S = a.S, SW = a.S + a.Wv;
+
   // last key visible to chunk row `row`: its own position (causal), or the
   // chunk's last key when the chunk attends to itself bidirectionally
   auto last_key_of_row = [&](int row) __attribute__((always_inline)) {
@@ -128,27 +103,18 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   const int row0 = rt * BM;
   const int n_tiles = tiles_of(rt);
 
-  // this wave: rows wrow0 + rb*32 + l32, rb < RB
-  const int wrow0 = row0 + wave * 32 * RB;
+  // this wave: rows wrow0 + l32
+  const int wrow0 = row0 + wave * 32;
   const bool wave_active = wrow0 < C;
   const int wave_first_lim = last_key_of_row(wrow0);              // last key of the wave's first row
-  const int wave_last_lim = last_key_of_row(wrow0 + 32 * RB - 1);
-  int key_lim[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) key_lim[rb] = last_key_of_row(wrow0 + rb * 32 + l32);
+  const int wave_last_lim = last_key_of_row(wrow0 + 31);
+  const int key_lim = last_key_of_row(wrow0 + l32);
 
-  // ---- Q rows of this wave as MFMA B fragments (lane: row l32, dims hh*8..+8)
-  bf16x8 qf[RB][NKS];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int row = wrow0 + rb * 32 + l32;
-    const uint16_t* qp = a.q + ((int64_t)min(row, C - 1) * a.Hq + h) * D + hh * 8;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const u32x4 v = (row < C) ? *(const u32x4*)(qp + ks * 16) : u32x4{0u, 0u, 0u, 0u};
-      qf[rb][ks] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
+  // ---- the wave's Q rows and running state.  The Q loads are unconditional:
+  // rows past the chunk end repeat the last row (the clamped address) and are
+  // never stored, and a row's softmax only mixes the two lanes of that row.
+  bf16x8 qf[WaveTile<D>::NKS];
+  WaveTile<D>::load_q(qf, a.q + ((int64_t)min(wrow0 + l32, C - 1) * a.Hq + h) * D + hh * 8);
 
   // ---- tile loader.  Direct load n of wave w fills LDS rows w*BN/4 + n*RPL ..
   // (RPL rows): lane i writes unit i % UPR of row w*BN/4 + n*RPL + i / UPR and
@@ -164,8 +130,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
     const int r = wave * (BN / NW) + n * RPL + lane / UPR;
     const int pu = lane % UPR;
     ld_row[n] = r;
-    ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ fk(r)) * 16);
-    ld_cv[n] = (uint32_t)(kv * D * 2 + (pu ^ fv(r)) * 16);
+    ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ lds_swz_k<D>(r)) * 16);
+    ld_cv[n] = (uint32_t)(kv * D * 2 + (pu ^ lds_swz_v<D>(r)) * 16);
   }
 
   // tile kind (wave-uniform): 0 sink, 1 ring without wrap, 2 chunk, all rows
@@ -239,150 +205,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
     return false;
   };
 
-  // per-lane LDS byte offsets of the MFMA operand reads
-  //   K fragment (kb, ks): row kb*32 + l32, logical unit 2*ks + hh
-  uint32_t k_rd[NKS];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) k_rd[ks] = (uint32_t)(l32 * RBY + (((2 * ks) | hh) ^ fk(l32)) * 16);
-  //   V^T fragment (db, kp, half): 16-lane group G = lane/16 covers dims
-  //   (G%2)*16 .. +15 of a 32-dim block and k-slots (G/2)*8 ..; its lane
-  //   4j+q supplies key j of the group's 4 keys (row kp*16 + half*8 +
-  //   (G/2)*4 + j), dims 4q .. 4q+3.
-  uint32_t v_rd[NDB];
-  {
-    const int j = (lane & 15) >> 2, q = lane & 3;
-    const int r = (lane >> 5) * 4 + j;            // row within the 8-row half-group (fv depends on r mod 4 only)
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const int u = db * 4 + ((lane >> 4) & 1) * 2 + (q >> 1);
-      v_rd[db] = (uint32_t)(r * RBY + (u ^ fv(r)) * 16 + (q & 1) * 8);
-    }
-  }
-
-  // ---- running state of this lane's rows (both halves hold the same m)
-  f32x16 o[RB][NDB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) o[rb][db] = f32x16{};
-  float m_run[RB], l_run[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) { m_run[rb] = -INFINITY; l_run[rb] = 0.f; }
-  const float c = a.scale_log2;
-
-  // Q K^T for one 32-key half of the tile: every K fragment feeds each row block
-  auto qk_half = [&](const uint16_t* Ks, int h, f32x16 (&s)[RB]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) s[rb] = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const bf16x8 kf = *(const bf16x8*)((const char*)Ks + h * 32 * RBY + k_rd[ks]);
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        s[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[rb][ks], s[rb], 0, 0, 0);
-    }
-  };
-  // causal mask of one half (diagonal tiles only)
-  auto mask_half = [&](int k0h, f32x16 (&s)[RB]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int kk = k0h + 8 * (v >> 2) + hh * 4 + (v & 3);
-        if (kk > key_lim[rb]) s[rb][v] = -INFINITY;
-      }
-  };
-  // Softmax of one half.  The probabilities are taken against the running
-  // max first (exp2, bf16 pack, lane sums), so the exponentials do not wait
-  // for a row-max reduction.  While no probability of the wave exceeds 2^8 (a
-  // lane's sum bounds each of its 16 terms) that max stays; otherwise, and
-  // while a row has no max yet, the max is raised to the half's row max, O and
-  // l are rescaled and the half is exponentiated again (rare, wave-uniform).
-  auto softmax_half = [&](const f32x16 (&s)[RB], bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
-    float lsum[RB];
-    auto expo = [&](int rb) __attribute__((always_inline)) {
-      const float neg_m = (m_run[rb] == -INFINITY) ? 0.f : -m_run[rb];
-      float e[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[rb][v], c, neg_m));
-      float s0 = 0.f, s1 = 0.f;      // two chains
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        s0 += e[2 * v];
-        s1 += e[2 * v + 1];
-      }
-#pragma unroll
-      for (int kp = 0; kp < 2; ++kp)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pf[rb][kp][j] = (__bf16)e[kp * 8 + j];
-      lsum[rb] = s0 + s1;
-    };
-    bool redo = false;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      expo(rb);
-      redo |= !(lsum[rb] <= kLaneSumLimit) || m_run[rb] == -INFINITY;
-    }
-    if (__builtin_amdgcn_ballot_w64(redo)) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[rb][v]);
-        // branch-free per lane: a divergent branch here would keep two copies of O
-        const float m_new = fmaxf(m_run[rb], pair_max(mx) * c);
-        const float alpha = (m_new == m_run[rb]) ? 1.f : __builtin_amdgcn_exp2f(m_run[rb] - m_new);
-        l_run[rb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[rb][db] *= alpha;
-        m_run[rb] = m_new;
-        expo(rb);
-      }
-    }
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) l_run[rb] += lsum[rb];
-  };
-  // O^T += V^T P^T for one half: every V^T fragment feeds each row block
-  auto pv_half = [&](const uint16_t* Vs, int h, const bf16x8 (&pf)[RB][2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int kp = 0; kp < 2; ++kp) {
-        const char* vp = (const char*)Vs + v_rd[db] + (h * 32 + kp * 16) * RBY;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * RBY));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[rb][kp], o[rb][db], 0, 0, 0);
-      }
-  };
-
-  // One 64-key tile in two 32-key halves, ordered so that the matrix cores
-  // multiply one half while the VALU exponentiates the other:
-  //   QK(0) | [QK(1) with softmax(0)] [PV(0) with softmax(1)] | PV(1)
-  // The wave raises its issue priority while it feeds the matrix cores, so of
-  // the two waves sharing a SIMD the one with MFMAs ready goes first and the
-  // other's softmax VALU work fills the MFMA shadow.
-  auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    f32x16 s0[RB], s1[RB];
-    bf16x8 p0[RB][2], p1[RB][2];
-    __builtin_amdgcn_s_setprio(1);
-    qk_half(Ks, 0, s0);
-    __builtin_amdgcn_s_setprio(0);
-    if constexpr (MASK) mask_half(k0, s0);
-    __builtin_amdgcn_s_setprio(1);
-    qk_half(Ks, 1, s1);
-    softmax_half(s0, p0);
-    pv_half(Vs, 0, p0);
-    if constexpr (MASK) mask_half(k0 + 32, s1);
-    __builtin_amdgcn_s_setprio(0);
-    softmax_half(s1, p1);
-    __builtin_amdgcn_s_setprio(1);
-    pv_half(Vs, 1, p1);
-    __builtin_amdgcn_s_setprio(0);
-  };
+  uint32_t k_rd[WaveTile<D>::NKS], v_rd[WaveTile<D>::NDB];
+  f32x16 o[WaveTile<D>::NDB];
+  float m_run, l_run;
+  WaveTile<D>::start(k_rd, v_rd, o, m_run, l_run);
+  WaveTile<D> wt{qf, k_rd, v_rd, o, m_run, l_run, a.scale_log2};
 
   // ---- key loop over the buffers: tile t + NBUF - 1 is loaded while tile t is
   // multiplied; one barrier per tile.
@@ -400,9 +227,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
       const uint16_t* Vs = vbuf(b) + sub * 64 * D;
       if (wave_active && k0 <= wave_last_lim) {
         if (k0 + 63 > wave_first_lim)
-          compute_tile(Ks, Vs, k0, std::true_type{});
+          wt.template tile<true>(Ks, Vs, k0, key_lim, hh);
         else
-          compute_tile(Ks, Vs, k0, std::false_type{});
+          wt.template tile<false>(Ks, Vs, k0, key_lim, hh);
       }
     }
     // Tile t + 1 must have landed.  With three buffers the newest tile's
@@ -427,53 +254,50 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   }
 
   if (!wave_active) return;
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int row = wrow0 + rb * 32 + l32;
-    const float l_tot = pair_sum(l_run[rb]);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float lse2 = l_tot > 0.f ? m_run[rb] + __log2f(l_tot) : -INFINITY;
-    if (row >= C) continue;
-    if (!partial) {
-      if (a.out_f32) {
-        float* op = (float*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const f32x16& x = o[rb][db];
-            *(f32x4*)(op + db * 32 + q4 * 8) =
-                f32x4{x[q4 * 4] * inv, x[q4 * 4 + 1] * inv, x[q4 * 4 + 2] * inv, x[q4 * 4 + 3] * inv};
-          }
-      } else {
-        __bf16* op = (__bf16*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const f32x16& x = o[rb][db];
-            *(bf16x4*)(op + db * 32 + q4 * 8) =
-                bf16x4{(__bf16)(x[q4 * 4] * inv), (__bf16)(x[q4 * 4 + 1] * inv), (__bf16)(x[q4 * 4 + 2] * inv),
-                       (__bf16)(x[q4 * 4 + 3] * inv)};
-          }
-      }
-      if (a.lse && hh == 0) a.lse[(int64_t)h * C + row] = lse2 * kLn2;
-    } else {
-      float* op = a.ws_o + (((int64_t)part * a.Hq + h) * C + row) * D + hh * 4;
+  constexpr int NDB = WaveTile<D>::NDB;
+  const int row = wrow0 + l32;
+  float inv, lse2;
+  wt.finish(inv, lse2);
+  if (row >= C) return;
+  if (!partial) {
+    if (a.out_f32) {
+      float* op = (float*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
-          const f32x16& x = o[rb][db];
+          const f32x16& x = o[db];
           *(f32x4*)(op + db * 32 + q4 * 8) =
               f32x4{x[q4 * 4] * inv, x[q4 * 4 + 1] * inv, x[q4 * 4 + 2] * inv, x[q4 * 4 + 3] * inv};
         }
-      if (hh == 0) {
-        a.ws_lse[((int64_t)part * a.Hq + h) * C + row] = lse2;
-        // a row tile that ends in this segment uses no later parts
-        if (t_hi == n_tiles)
-          for (int p2 = part + 1; p2 < n_parts; ++p2) a.ws_lse[((int64_t)p2 * a.Hq + h) * C + row] = -INFINITY;
+    } else {
+      __bf16* op = (__bf16*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const f32x16& x = o[db];
+          *(bf16x4*)(op + db * 32 + q4 * 8) =
+              bf16x4{(__bf16)(x[q4 * 4] * inv), (__bf16)(x[q4 * 4 + 1] * inv), (__bf16)(x[q4 * 4 + 2] * inv),
+                     (__bf16)(x[q4 * 4 + 3] * inv)};
+        }
+    }
+    if (a.lse && hh == 0) a.lse[(int64_t)h * C + row] = lse2 * kLn2;
+  } else {
+    float* op = a.ws_o + (((int64_t)part * a.Hq + h) * C + row) * D + hh * 4;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const f32x16& x = o[db];
+        *(f32x4*)(op + db * 32 + q4 * 8) =
+            f32x4{x[q4 * 4] * inv, x[q4 * 4 + 1] * inv, x[q4 * 4 + 2] * inv, x[q4 * 4 + 3] * inv};
       }
+    if (hh == 0) {
+      a.ws_lse[((int64_t)part * a.Hq + h) * C + row] = lse2;
+      // a row tile that ends in this segment uses no later parts
+      if (t_hi == n_tiles)
+        for (int p2 = part + 1; p2 < n_parts; ++p2) a.ws_lse[((int64_t)p2 * a.Hq + h) * C + row] = -INFINITY;
     }
   }
   };   // segment

@@ -16,8 +16,8 @@
 //     rows per KV head, and a 32-token query 7*32 = 224 rows: one 256-row
 //     work-group of 8 waves reads each K/V tile once for all of them.
 //   * The tile body (MFMA S^T = K Q^T, online softmax, O^T = V^T P^T with the
-//     transposing LDS read, two 32-key halves) is the one of the chunk
-//     prefill kernel.
+//     transposing LDS read, two 32-key halves) is WaveTile of attn_common.h,
+//     shared with the chunk prefill kernel.
 //   * Keys are walked in 64-key tiles, double-buffered in LDS.  A tile inside
 //     the gathered region is loaded straight from HBM into LDS with a slot
 //     resolved per lane (the store is one buffer resource, so the rows of a
@@ -42,7 +42,6 @@ template <int D>
 __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherArgs a) {
   constexpr int BN = 64;
   constexpr int BM = kGatherThreads / 64 * 32;
-  constexpr int NKS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int UPR = D / 8;
   constexpr int RBY = D * 2;
@@ -54,8 +53,6 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
   static_assert(NLD * NW * 1024 == BN * RBY, "direct loads cover the tile");
   static_assert(BM == NW * 32, "one 32-row block per wave");
   static_assert(SEG_PER_THREAD * kGatherThreads == kMaxSegments, "segment table split");
-  auto fk = [](int r) __attribute__((always_inline)) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
-  auto fv = [](int r) __attribute__((always_inline)) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); };
 
   // NBUF K/V buffers, tile t in buffer t mod NBUF, loaded NBUF-1 tiles ahead:
   // this kernel is bound by HBM, so three tiles stay in flight per work-group.
@@ -103,12 +100,8 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
   // branches, or a later fix-up of their values, leave the compiler unsure
   // whether they completed, and it then waits for every load in flight.)
   // Issued first, so that the wait for the segment table covers them.
-  bf16x8 qf[NKS];
-  {
-    const uint16_t* qp = a.q + ((int64_t)my_tok * a.Hq + my_head) * D + hh * 8;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + ks * 16));
-  }
+  bf16x8 qf[WaveTile<D>::NKS];
+  WaveTile<D>::load_q(qf, a.q + ((int64_t)my_tok * a.Hq + my_head) * D + hh * 8);
 
   // ---- segment table: clamp every segment to the store, prefix-sum lengths
   {
@@ -193,8 +186,8 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
     const int r = wave * (BN / NW) + n * RPL + lane / UPR;
     const int pu = lane % UPR;
     ld_row[n] = r;
-    ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ fk(r)) * 16);
-    ld_cv[n] = (uint32_t)(kv * D * 2 + (pu ^ fv(r)) * 16);
+    ld_ck[n] = (uint32_t)(kv * D * 2 + (pu ^ lds_swz_k<D>(r)) * 16);
+    ld_cv[n] = (uint32_t)(kv * D * 2 + (pu ^ lds_swz_v<D>(r)) * 16);
   }
 
   // tile kind (wave-uniform): 0 sink, 1 gathered, 2 tail (all rows inside); 3 mixed
@@ -251,109 +244,11 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
     return false;
   };
 
-  uint32_t k_rd[NKS];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) k_rd[ks] = (uint32_t)(l32 * RBY + (((2 * ks) | hh) ^ fk(l32)) * 16);
-  uint32_t v_rd[NDB];
-  {
-    const int j = (lane & 15) >> 2, q = lane & 3;
-    const int r = (lane >> 5) * 4 + j;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const int u = db * 4 + ((lane >> 4) & 1) * 2 + (q >> 1);
-      v_rd[db] = (uint32_t)(r * RBY + (u ^ fv(r)) * 16 + (q & 1) * 8);
-    }
-  }
-
-  f32x16 o[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) o[db] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
-  const float c = a.scale_log2;
-
-  auto qk_half = [&](const uint16_t* Ks, int h, f32x16& s) __attribute__((always_inline)) {
-    s = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const bf16x8 kf = *(const bf16x8*)((const char*)Ks + h * 32 * RBY + k_rd[ks]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
-    }
-  };
-  auto mask_half = [&](int k0h, f32x16& s) __attribute__((always_inline)) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int kk = k0h + 8 * (v >> 2) + hh * 4 + (v & 3);
-      if (kk > key_lim) s[v] = -INFINITY;
-    }
-  };
-  // Softmax of one half against the running max, as in the chunk kernel:
-  // exponentiate first; raise the max (rescale O and l, redo the half) only
-  // when a lane's sum of its 16 probabilities exceeds 2^8 or the row has no
-  // max yet.
-  auto softmax_half = [&](const f32x16& s, bf16x8 (&pf)[2]) __attribute__((always_inline)) {
-    auto expo = [&]() __attribute__((always_inline)) {
-      const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
-      float e[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, neg_m));
-      float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        s0 += e[2 * v];
-        s1 += e[2 * v + 1];
-      }
-#pragma unroll
-      for (int kp = 0; kp < 2; ++kp)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pf[kp][j] = (__bf16)e[kp * 8 + j];
-      return s0 + s1;
-    };
-    float lsum = expo();
-    if (__builtin_amdgcn_ballot_w64(!(lsum <= kLaneSumLimit) || m_run == -INFINITY)) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[v]);
-      const float m_new = fmaxf(m_run, pair_max(mx) * c);
-      const float alpha = (m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-      m_run = m_new;
-      lsum = expo();
-    }
-    l_run += lsum;
-  };
-  auto pv_half = [&](const uint16_t* Vs, int h, const bf16x8 (&pf)[2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int kp = 0; kp < 2; ++kp) {
-        const char* vp = (const char*)Vs + v_rd[db] + (h * 32 + kp * 16) * RBY;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * RBY));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kp], o[db], 0, 0, 0);
-      }
-  };
-  auto compute_tile = [&](const uint16_t* Ks, const uint16_t* Vs, int k0, auto mask_tag) __attribute__((always_inline)) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    f32x16 s0, s1;
-    bf16x8 p0[2], p1[2];
-    __builtin_amdgcn_s_setprio(1);
-    qk_half(Ks, 0, s0);
-    __builtin_amdgcn_s_setprio(0);
-    if constexpr (MASK) mask_half(k0, s0);
-    __builtin_amdgcn_s_setprio(1);
-    qk_half(Ks, 1, s1);
-    softmax_half(s0, p0);
-    pv_half(Vs, 0, p0);
-    if constexpr (MASK) mask_half(k0 + 32, s1);
-    __builtin_amdgcn_s_setprio(0);
-    softmax_half(s1, p1);
-    __builtin_amdgcn_s_setprio(1);
-    pv_half(Vs, 1, p1);
-    __builtin_amdgcn_s_setprio(0);
-  };
+  uint32_t k_rd[WaveTile<D>::NKS], v_rd[WaveTile<D>::NDB];
+  f32x16 o[WaveTile<D>::NDB];
+  float m_run, l_run;
+  WaveTile<D>::start(k_rd, v_rd, o, m_run, l_run);
+  WaveTile<D> wt{qf, k_rd, v_rd, o, m_run, l_run, a.scale_log2};
 
   // Key loop.  Step t computes tile t while tiles t+1 .. t+NBUF-1 load; it
   // then waits for tile t+1 only: the direct loads of the newer tiles (each
@@ -371,9 +266,9 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
     const int k0 = t * BN;
     if (wave_active && k0 <= wave_last_lim) {
       if (k0 + BN - 1 > wave_first_lim)
-        compute_tile(kbuf(b), vbuf(b), k0, std::true_type{});
+        wt.template tile<true>(kbuf(b), vbuf(b), k0, key_lim, hh);
       else
-        compute_tile(kbuf(b), vbuf(b), k0, std::false_type{});
+        wt.template tile<false>(kbuf(b), vbuf(b), k0, key_lim, hh);
     }
     const int n_newer = (newer_async ? 1 : 0) + (an ? 1 : 0);
     if (n_newer == 2) __builtin_amdgcn_s_waitcnt(kWait2);
@@ -402,9 +297,8 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
   }
 
   if (!wave_active || my_row >= NR) return;
-  const float l_tot = pair_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse2 = l_tot > 0.f ? m_run + __log2f(l_tot) : -INFINITY;
+  float inv, lse2;
+  wt.finish(inv, lse2);
   const int64_t orow = (int64_t)my_tok * a.Hq + my_head;
   if (a.parts == 1) {
     if (a.out_f32) {
