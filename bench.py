@@ -275,6 +275,8 @@ def run_chunk_workload(args, torch, vico):
     n_warm = 0
     for cache in ("warm", "flushed"):
         for phase, H_of in phases.items():
+            if args.only_variant and args.only_variant != f"{cache}_{phase}":
+                continue
             ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(K)]
             fev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(2)) for _ in range(K)]
             # each variant is warmed up on its own steps right before it is timed: an idle
@@ -692,6 +694,8 @@ def main():
     ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append", "query", "decode",
                                                           "drop"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only-variant", default=None,
+                    help="chunk workloads: time only this variant (e.g. warm_wrapped), for profiling runs")
     ap.add_argument("--ramp", action="store_true",
                     help="instead of the benchmark: chunk attention time against time since an idle period")
     ap.add_argument("--cpu-rows", type=int, default=2048)

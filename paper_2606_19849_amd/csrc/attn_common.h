@@ -107,6 +107,7 @@ struct WaveTile {
   f32x16 (&o)[NDB];              // O^T accumulators
   float& m_run;                  // running max (log2 units) of this lane's row
   float& l_run;                  // this lane's sum of probabilities
+  float& neg_m;                  // -m_run, or 0 while m_run is -inf
   const float c;                 // softmax scale * log2(e)
 
   // Loads this lane's Q row (bf16, 16-byte aligned, at dims 8*(lane/32)) as
@@ -118,7 +119,7 @@ struct WaveTile {
 
   // Per-lane LDS byte offsets of the operand reads and an empty running state.
   __device__ __forceinline__ static void start(uint32_t (&krd)[NKS], uint32_t (&vrd)[NDB], f32x16 (&acc)[NDB],
-                                               float& m, float& l) {
+                                               float& m, float& l, float& nm) {
     const int lane = threadIdx.x & 63, l32 = lane & 31, hh = lane >> 5;
     //   K fragment (half h, ks): row h*32 + l32, logical unit 2*ks + hh
 #pragma unroll
@@ -138,6 +139,7 @@ struct WaveTile {
     for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
     m = -INFINITY;
     l = 0.f;
+    nm = 0.f;
   }
 
   // Q K^T for one 32-key half of the tile
@@ -169,13 +171,12 @@ struct WaveTile {
   // wave-uniform branch).
   __device__ __forceinline__ void softmax_half(const f32x16& s, bf16x8 (&pf)[2]) {
     auto expo = [&]() __attribute__((always_inline)) {
-      const float neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
       float e[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, neg_m));
-      float s0 = 0.f, s1 = 0.f;      // two chains
+      float s0 = e[0], s1 = e[1];    // two chains
 #pragma unroll
-      for (int v = 0; v < 8; ++v) {
+      for (int v = 1; v < 8; ++v) {
         s0 += e[2 * v];
         s1 += e[2 * v + 1];
       }
@@ -197,6 +198,7 @@ struct WaveTile {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) o[db] *= alpha;
       m_run = m_new;
+      neg_m = (m_new == -INFINITY) ? 0.f : -m_new;
       lsum = expo();
     }
     l_run += lsum;

@@ -207,9 +207,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
 
   uint32_t k_rd[WaveTile<D>::NKS], v_rd[WaveTile<D>::NDB];
   f32x16 o[WaveTile<D>::NDB];
-  float m_run, l_run;
-  WaveTile<D>::start(k_rd, v_rd, o, m_run, l_run);
-  WaveTile<D> wt{qf, k_rd, v_rd, o, m_run, l_run, a.scale_log2};
+  float m_run, l_run, neg_m;
+  WaveTile<D>::start(k_rd, v_rd, o, m_run, l_run, neg_m);
+  WaveTile<D> wt{qf, k_rd, v_rd, o, m_run, l_run, neg_m, a.scale_log2};
 
   // ---- key loop over the buffers: tile t + NBUF - 1 is loaded while tile t is
   // multiplied; one barrier per tile.

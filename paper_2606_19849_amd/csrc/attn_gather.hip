@@ -246,9 +246,9 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
 
   uint32_t k_rd[WaveTile<D>::NKS], v_rd[WaveTile<D>::NDB];
   f32x16 o[WaveTile<D>::NDB];
-  float m_run, l_run;
-  WaveTile<D>::start(k_rd, v_rd, o, m_run, l_run);
-  WaveTile<D> wt{qf, k_rd, v_rd, o, m_run, l_run, a.scale_log2};
+  float m_run, l_run, neg_m;
+  WaveTile<D>::start(k_rd, v_rd, o, m_run, l_run, neg_m);
+  WaveTile<D> wt{qf, k_rd, v_rd, o, m_run, l_run, neg_m, a.scale_log2};
 
   // Key loop.  Step t computes tile t while tiles t+1 .. t+NBUF-1 load; it
   // then waits for tile t+1 only: the direct loads of the newer tiles (each
