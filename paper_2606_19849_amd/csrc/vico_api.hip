@@ -41,18 +41,19 @@ int64_t tiles_of(int rt, int C, int SW, int bidir) {
   return (SW + last + vico::kKeyTile - 1) / vico::kKeyTile;
 }
 
-// Splits of every row tile's key range (power of two), chosen while the grid
-// stays within one round of resident work-groups and each split keeps at
-// least 16 key tiles.
+// Splits of every row tile's key range: as many as keep the grid within one
+// round of resident work-groups (so that, e.g., 48 row tiles take 5 splits
+// and fill 240 of the 256 CUs), with at least 16 key tiles per split and at
+// most kAutoSplits.
 int plan_splits(int C, int S, int Wv, int Hq, int request) {
   const int64_t n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
   const int64_t wgs = int64_t(Hq) * n_rt;
   const int64_t tiles = (int64_t(S) + Wv + C + vico::kKeyTile - 1) / vico::kKeyTile;
   const int64_t cap = tiles < vico::kMaxSplits ? tiles : vico::kMaxSplits;
   if (request > 0) return (int)(request < cap ? request : cap);
-  int ns = 1;
-  while (ns * 2 <= cap && wgs * ns * 2 <= int64_t(vico::kNumCUs) * vico::kWgPerCU && tiles >= 16 * ns * 2) ns *= 2;
-  return ns;
+  int64_t ns = int64_t(vico::kNumCUs) * vico::kWgPerCU / wgs;
+  ns = std::min<int64_t>(std::min<int64_t>(ns, vico::kAutoSplits), std::min<int64_t>(cap, tiles / 16));
+  return (int)std::max<int64_t>(ns, 1);
 }
 
 // Balanced plan: gridDim.x equal shares of the (row tile, key tile) pairs.

@@ -19,6 +19,7 @@ constexpr int kBuffers = 2;
 constexpr int kNumCUs = 256;        // MI355X: 8 XCDs x 32 CUs
 constexpr int kWgPerCU = 1;
 constexpr int kMaxSplits = 16;
+constexpr int kAutoSplits = 8;      // most key splits the planner picks by itself (the merge reads up to 8 parts at once)
 
 
 // Everything the attention kernels need, resolved on the host.
