@@ -135,7 +135,7 @@ DESCR = {
     "3b": "qwen2.5-vl-3b layer chunk prefill: 16q/2kv heads, d128, sink 64, W=R=8192, chunk 1024",
     "full": "3b heads, full history 65536 + sink 64, chunk 2048 (unbounded control)",
     "full_bounded": "3b heads, history 65536 + sink 64, W=8192, chunk 2048",
-    "stream": "3b heads, 64 chunks ragged in [256,1024], sink 64, W=R=8192, attend then append",
+    "stream": "3b heads, 64 chunks ragged in [256,1024], sink 64, W=R=8192, attend then append (one call per chunk)",
     "query": "qwen2.5-vl-7b query-side path per layer: mean of a 32-token query, cosine over 256 stored chunk "
              "features (dm 3584), top-32 chunks, attention of 32 query rows over sink 64 + retrieved chunks "
              "(256..1024 tokens each) + causal query; 28q/4kv, d128; 8 queries in rotation",
@@ -430,10 +430,10 @@ def run_stream_workload(args, torch, vico):
             for t, c in enumerate(counts):
                 q, k, v = chunks[t]
                 ev[t][0].record(stream)
+                # attend, then append the chunk to the ring, in one call
                 vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, int(starts[t]), window, outs[t],
-                                             workspace=ws, stream=stream)
+                                             workspace=ws, stream=stream, flags=vico.VICO_ATTN_APPEND)
                 ev[t][1].record(stream)
-                vico.vico_kv_append(k, v, rk, rv, int(starts[t]), stream=stream)
                 ev[t][2].record(stream)
             torch.cuda.synchronize()
             if n_warm is not None:

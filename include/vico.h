@@ -59,6 +59,7 @@ enum { VICO_DTYPE_BF16 = 0, VICO_DTYPE_F32 = 1 };
 #define VICO_SPLIT_BALANCED (-1)
 /* flags of the _ex entry points */
 #define VICO_ATTN_BIDIRECTIONAL 1  /* every chunk row sees the whole chunk (no causal mask) */
+#define VICO_ATTN_APPEND 2         /* then append the chunk's K/V to the ring (as vico_kv_append) */
 
 /*
  * vico_kv_append -- append a chunk's K/V to the ring-buffer visual cache.
@@ -132,7 +133,13 @@ int vico_chunk_prefill_attn(const void* q, const void* k_chunk, const void* v_ch
  * flags = 0 is vico_chunk_prefill_attn.  VICO_ATTN_BIDIRECTIONAL: the
  * additive mask of Eq. (4) read literally -- a vision token sees every token
  * of the chunks in its window, its own chunk included -- so row i sees
- * chunk[0 .. chunk_len) instead of chunk[0 .. i].  Other bits are invalid.
+ * chunk[0 .. chunk_len) instead of chunk[0 .. i].  VICO_ATTN_APPEND: after
+ * attending, the call also does what vico_kv_append(k_chunk, v_chunk, ...,
+ * hist_len) would (the ring of Sec. 3 advances by the chunk), after every
+ * read of the window: the split-merge kernel copies the chunk alongside the
+ * merge, so a split call saves a launch; without a split the copy is its own
+ * launch.  It needs ring_k/ring_v, chunk_len <= ring_slots, and chunk buffers
+ * that do not overlap the ring (as vico_kv_append).  Other bits are invalid.
  * Use vico_attn_plan_ex with the same flags for the workspace size.
  *
  * The paper's window is whole chunks (the most recent acn chunks, the

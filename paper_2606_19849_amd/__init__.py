@@ -17,6 +17,7 @@ from ._binding import (
     VICO_FULL_HISTORY,
     VICO_SPLIT_BALANCED,
     VICO_ATTN_BIDIRECTIONAL,
+    VICO_ATTN_APPEND,
     VICO_NOALLOC_SCRATCH_BYTES,
     VicoError,
     load_library,
@@ -41,6 +42,7 @@ __all__ = [
     "VICO_FULL_HISTORY",
     "VICO_SPLIT_BALANCED",
     "VICO_ATTN_BIDIRECTIONAL",
+    "VICO_ATTN_APPEND",
     "VICO_NOALLOC_SCRATCH_BYTES",
     "VicoError",
     "load_library",

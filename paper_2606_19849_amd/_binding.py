@@ -22,6 +22,7 @@ VICO_DTYPE_F32 = 1
 VICO_FULL_HISTORY = -1
 VICO_SPLIT_BALANCED = -1
 VICO_ATTN_BIDIRECTIONAL = 1
+VICO_ATTN_APPEND = 2
 VICO_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _i32, _i64, _f32, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p

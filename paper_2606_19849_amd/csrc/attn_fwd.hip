@@ -365,8 +365,11 @@ hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream) {
   else
     hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a, n_rt, g);
   hipError_t err = hipGetLastError();
-  if (err != hipSuccess || a.splits == 1) return err;
-  return launch_merge(a, stream);
+  if (err != hipSuccess) return err;
+  if (a.splits > 1) return launch_merge(a, stream);   // appends too, when asked
+  if (!a.app_rk) return err;
+  const AppendArgs ap{a.kc, a.vc, a.app_rk, a.app_rv, a.C, a.R, a.app_p0, a.Hkv * a.D};
+  return launch_append(ap, stream);
 }
 
 }  // namespace vico

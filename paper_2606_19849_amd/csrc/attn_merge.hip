@@ -14,6 +14,8 @@
 // loads of a row are then in flight together.  The part weights come from
 // one wave-wide max and sum over the parts (lane = part).
 
+#include <algorithm>
+
 #include "attn_common.h"
 
 namespace vico {
@@ -22,11 +24,23 @@ namespace {
 constexpr int kMergeThreads = 256;
 constexpr int kFewParts = 8;     // up to here one thread per (row, 4 columns) loads all parts
 
+// With an append requested, the blocks past `merge_blocks` copy the chunk's
+// K/V into the ring instead of merging: this launch runs after every read of
+// the window, so the ring slots it overwrites are free.
+__device__ __forceinline__ bool append_block(const AttnArgs& a, int merge_blocks) {
+  if ((int)blockIdx.x < merge_blocks) return false;
+  const AppendArgs ap{a.kc, a.vc, a.app_rk, a.app_rv, a.C, a.R, a.app_p0, a.Hkv * a.D};
+  const int64_t n = (int64_t)(gridDim.x - merge_blocks) * blockDim.x;
+  append_units(ap, (int64_t)(blockIdx.x - merge_blocks) * blockDim.x + threadIdx.x, n);
+  return true;
+}
+
 // Few parts, many rows (chunk prefill splits): one thread per (head, row,
 // 4-column group) reads every part's value at once; neighbouring threads
 // read neighbouring columns, so every load is a full coalesced row.
 template <int D>
-__global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs a, int merge_blocks) {
+  if (append_block(a, merge_blocks)) return;
   constexpr int NQ = D / 4;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n_rows = (int64_t)a.Hq * a.C;
@@ -70,7 +84,8 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs
 // Many parts (short queries): see the file comment.
 
 template <int D>
-__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a, int PG, int RPB) {
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a, int PG, int RPB, int merge_blocks) {
+  if (append_block(a, merge_blocks)) return;      // whole blocks: before any barrier
   constexpr int NQ = D / 4;                       // float4 columns per row
   __shared__ float w_s[kMergeThreads / NQ][64];   // per row of the block: part weights
   __shared__ float inv_s[kMergeThreads / NQ];
@@ -136,12 +151,17 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a, i
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
   if (a.splits < 1 || a.splits > 64) return hipErrorInvalidValue;   // one wave holds the part weights
   const int64_t rows = (int64_t)a.Hq * a.C;
+  // copy blocks for the append (one 16-byte unit per thread per step)
+  const int64_t app_units = a.app_rk ? 2 * (int64_t)a.C * (a.Hkv * a.D / 8) : 0;
+  const int app_blocks = (int)std::min<int64_t>((app_units + kMergeThreads - 1) / kMergeThreads, 2048);
   if (a.splits <= kFewParts) {
     const int blocks = (int)((rows * (a.D / 4) + kMergeThreads - 1) / kMergeThreads);
     if (a.D == 128)
-      hipLaunchKernelGGL(attn_merge_rows_kernel<128>, dim3(blocks), dim3(kMergeThreads), 0, stream, a);
+      hipLaunchKernelGGL(attn_merge_rows_kernel<128>, dim3(blocks + app_blocks), dim3(kMergeThreads), 0, stream, a,
+                         blocks);
     else
-      hipLaunchKernelGGL(attn_merge_rows_kernel<64>, dim3(blocks), dim3(kMergeThreads), 0, stream, a);
+      hipLaunchKernelGGL(attn_merge_rows_kernel<64>, dim3(blocks + app_blocks), dim3(kMergeThreads), 0, stream, a,
+                         blocks);
     return hipGetLastError();
   }
   // part groups: the parts rounded up to a power of two, at most what one row's
@@ -152,9 +172,11 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
   const int rpb = kMergeThreads / (nq * pg);
   const int blocks = (int)((rows + rpb - 1) / rpb);
   if (a.D == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(blocks), dim3(kMergeThreads), 0, stream, a, pg, rpb);
+    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(blocks + app_blocks), dim3(kMergeThreads), 0, stream, a, pg, rpb,
+                       blocks);
   else
-    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(blocks), dim3(kMergeThreads), 0, stream, a, pg, rpb);
+    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(blocks + app_blocks), dim3(kMergeThreads), 0, stream, a, pg, rpb,
+                       blocks);
   return hipGetLastError();
 }
 

@@ -5,7 +5,9 @@
 // Prefilling and Decoding").  Token rows are contiguous, so the destination
 // is at most two contiguous runs of slots; each thread moves one 16-byte
 // unit with one load and one store, consecutive threads consecutive units:
-// fully coalesced on both sides.  The wrap is one compare-and-subtract.
+// fully coalesced on both sides.  The wrap is one compare-and-subtract.  (The
+// split merge performs the same copy with append_units when an attention call
+// appends its chunk.)
 
 #include "vico_internal.h"
 
@@ -14,6 +16,7 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// blockIdx.y picks K (0) or V (1), so source and destination stay scalar
 __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   const int upt = a.row_elems >> 3;                  // 16-byte units per token row
   const int64_t total = (int64_t)a.C * upt;

@@ -88,7 +88,7 @@ int plan_balanced(int C, int SW, int Hq, int Hkv, int bidir, int64_t* total, int
 int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int32_t Hq, int32_t Hkv,
                      int32_t D, int32_t splits, int32_t flags, Shape* sh) {
   if (C < 0 || S < 0 || R < 0 || H < 0 || W < -1 || splits < VICO_SPLIT_BALANCED) return VICO_ERR_INVALID_ARG;
-  if (flags & ~VICO_ATTN_BIDIRECTIONAL) return VICO_ERR_INVALID_ARG;
+  if (flags & ~(VICO_ATTN_BIDIRECTIONAL | VICO_ATTN_APPEND)) return VICO_ERR_INVALID_ARG;
   const int bidir = (flags & VICO_ATTN_BIDIRECTIONAL) ? 1 : 0;
   if (Hq < 1 || Hkv < 1 || Hq > kMaxHeads || Hq % Hkv != 0) return VICO_ERR_INVALID_ARG;
   if (D != 64 && D != 128) return VICO_ERR_UNSUPPORTED;
@@ -257,6 +257,9 @@ int vico_chunk_prefill_attn_ex(const void* q, const void* k_chunk, const void* v
   if (!q || !k_chunk || !v_chunk || !out) return VICO_ERR_INVALID_ARG;
   if (sh.S > 0 && (!sink_k || !sink_v)) return VICO_ERR_INVALID_ARG;
   if (sh.Wv > 0 && (!ring_k || !ring_v)) return VICO_ERR_INVALID_ARG;
+  const bool append = (flags & VICO_ATTN_APPEND) != 0;
+  if (append && (!ring_k || !ring_v)) return VICO_ERR_INVALID_ARG;
+  if (append && chunk_len > ring_slots) return VICO_ERR_CAPACITY;
   const void* ptrs[] = {q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v, out, workspace};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return VICO_ERR_MISALIGNED;
@@ -270,11 +273,22 @@ int vico_chunk_prefill_attn_ex(const void* q, const void* k_chunk, const void* v
   const int64_t rb = int64_t(ring_slots) * num_kv_heads * head_dim * 2;
   const int64_t lb = lse_out ? int64_t(num_q_heads) * chunk_len * 4 : 0;
   const void* ins[] = {q, k_chunk, v_chunk, sink_k, sink_v, ring_k, ring_v};
-  const int64_t inb[] = {qb, cb, cb, sb, sb, sh.Wv ? rb : 0, sh.Wv ? rb : 0};
+  const int64_t inb[] = {qb, cb, cb, sb, sb, (sh.Wv || append) ? rb : 0, (sh.Wv || append) ? rb : 0};
   for (int i = 0; i < 7; ++i)
     if (ins[i] && (overlaps(out, ob, ins[i], inb[i]) || overlaps(lse_out, lb, ins[i], inb[i])))
       return VICO_ERR_INVALID_ARG;
   if (overlaps(out, ob, lse_out, lb)) return VICO_ERR_INVALID_ARG;
+  // the append writes the ring: it must not alias the chunk, the other ring
+  // tensor, or the workspace the merge reads in the same launch
+  if (append) {
+    const int64_t wsb = sh.splits > 1 ? sh.ws_bytes : 0;
+    const void* other[] = {q, k_chunk, v_chunk, sink_k, sink_v, workspace};
+    const int64_t otb[] = {qb, cb, cb, sb, sb, wsb};
+    for (int i = 0; i < 6; ++i)
+      if (other[i] && (overlaps(ring_k, rb, other[i], otb[i]) || overlaps(ring_v, rb, other[i], otb[i])))
+        return VICO_ERR_INVALID_ARG;
+    if (overlaps(ring_k, rb, ring_v, rb)) return VICO_ERR_INVALID_ARG;
+  }
 
   vico::AttnArgs a{};
   a.q = (const uint16_t*)q;
@@ -297,6 +311,11 @@ int vico_chunk_prefill_attn_ex(const void* q, const void* k_chunk, const void* v
   a.total_tiles = sh.total_tiles;
   a.out_f32 = out_dtype == VICO_DTYPE_F32;
   a.bidir = sh.bidir;
+  if (append) {
+    a.app_rk = (uint16_t*)ring_k;
+    a.app_rv = (uint16_t*)ring_v;
+    a.app_p0 = (int)(hist_len % ring_slots);
+  }
   const double scale = softmax_scale > 0.f ? double(softmax_scale) : 1.0 / sqrt(double(head_dim));
   a.scale_log2 = (float)(scale * 1.4426950408889634);
   const hipError_t e = vico::launch_attention(a, sh.grid, (hipStream_t)stream);

@@ -43,6 +43,9 @@ struct AttnArgs {
   int out_f32;
   int bidir;           // 1: every chunk row sees the whole chunk (no causal mask)
   float scale_log2;    // softmax scale * log2(e)
+  uint16_t* app_rk;    // append after attending (null: no append): ring K, V
+  uint16_t* app_rv;
+  int app_p0;          // first ring slot written = hist_len mod R
 };
 
 // Short-query attention over gathered key segments: query rows are the last
@@ -92,6 +95,27 @@ struct AppendArgs {
   int C, R, p0;        // p0 = hist_len mod R
   int row_elems;       // Hkv * D
 };
+
+// The append of a chunk, ring[(p0 + j) mod R] <- chunk[j] for K and V, as
+// 16-byte units: unit u in [0, 2*C*row_elems/8) (K units first, then V);
+// threads take units first, first + stride, ...  Consecutive threads move
+// consecutive units, so loads and stores are coalesced.
+__device__ __forceinline__ void append_units(const AppendArgs& a, int64_t first, int64_t stride) {
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  const int upt = a.row_elems >> 3;                  // 16-byte units per token row
+  const int64_t per = (int64_t)a.C * upt;
+  for (int64_t u = first; u < 2 * per; u += stride) {
+    const bool v = u >= per;
+    const int64_t w = v ? u - per : u;
+    const int j = (int)(w / upt);
+    const int c = (int)(w - (int64_t)j * upt);
+    int slot = a.p0 + j;
+    if (slot >= a.R) slot -= a.R;
+    const uint16_t* src = v ? a.vc : a.kc;
+    uint16_t* dst = v ? a.rv : a.rk;
+    *(u32x4_t*)(dst + (int64_t)slot * a.row_elems + c * 8) = *(const u32x4_t*)(src + (int64_t)j * a.row_elems + c * 8);
+  }
+}
 
 hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream);
 // Merge of split key ranges (reads ws_o / ws_lse of `splits` parts, C rows per head).

@@ -324,7 +324,7 @@ def test_gather_plan_parts():
 
 def test_unknown_attention_flags_are_rejected():
     st = lib.vico_chunk_prefill_attn_ex(A, A + 0x100000, A + 0x200000, 64, A + 0x300000, A + 0x400000, 16,
-                                        A + 0x500000, A + 0x600000, 256, 456, 256, 2, 1, 64, 0.0, B, 1, None, 0, 2,
+                                        A + 0x500000, A + 0x600000, 256, 456, 256, 2, 1, 64, 0.0, B, 1, None, 0, 4,
                                         None, 0, None)
     assert st == -1
     assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, 0, 1) == vico.vico_attn_plan(64, 16, 256, 456,
@@ -350,6 +350,29 @@ def test_acn_window_rejects_bad_tables():
     assert lib.vico_acn_window(arr, 3, -1, 1) == -1
     assert lib.vico_acn_window(None, 3, 1, 1) == -1
     assert lib.vico_acn_window(arr, 3, 2, 1) == -1          # decreasing starts
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(C=300, R=256, W=200), -3),                 # the appended chunk is longer than the ring
+    (dict(rk=None, rv=None, W=0, H=0), -1),          # nothing to append to
+    (dict(kc=A + 0x500000), -1),                     # the chunk's K inside the ring the append writes
+    (dict(ws=A + 0x600000, wsb=1 << 30, splits=2), -1),   # the merge's workspace inside the ring
+])
+def test_attention_append_rejects_bad_arguments(kw, status):
+    a = dict(q=A, kc=A + 0x100000, vc=A + 0x200000, C=64, sk=A + 0x300000, sv=A + 0x400000, S=16,
+             rk=A + 0x500000, rv=A + 0x600000, R=256, H=456, W=256, Hq=2, Hkv=1, D=64, scale=0.0,
+             out=B, odt=1, lse=None, splits=0, ws=None, wsb=0)
+    a.update(kw)
+    st = lib.vico_chunk_prefill_attn_ex(a["q"], a["kc"], a["vc"], a["C"], a["sk"], a["sv"], a["S"], a["rk"], a["rv"],
+                                        a["R"], a["H"], a["W"], a["Hq"], a["Hkv"], a["D"], a["scale"], a["out"],
+                                        a["odt"], a["lse"], a["splits"], vico.VICO_ATTN_APPEND, a["ws"], a["wsb"],
+                                        None)
+    assert st == status
+
+
+def test_append_flag_is_accepted_by_the_plan():
+    assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, 0, vico.VICO_ATTN_APPEND) == \
+        vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64)
 
 
 def test_balanced_plan_counts_whole_chunks_when_bidirectional():

@@ -65,3 +65,45 @@ def test_ragged_stream_of_appends():
     lin = np.concatenate(lin_k)
     got = bits_of(rk)
     assert np.array_equal(got[np.arange(H - R, H) % R], lin[H - R:H])
+
+
+@pytest.mark.parametrize("splits,flags", [(0, 0), (1, 0), (4, 0), (12, 0), (0, vico.VICO_ATTN_BIDIRECTIONAL)])
+def test_attention_with_append_equals_attention_then_append(splits, flags):
+    """VICO_ATTN_APPEND: one call attends and then appends (the copy rides on
+    the split merge, or runs as its own launch without a split).  Over a
+    stream of ragged chunks through a ring that wraps, outputs, LSE and the
+    ring must equal, bit for bit, an attention call followed by
+    vico_kv_append on a second ring; the ring must also equal the oracle's
+    ring model."""
+    Hq, Hkv, D, S, R, W = 8, 2, 128, 16, 1024, 1024
+    rng = np.random.default_rng(70 + splits + flags)
+    counts = [300, 513, 64, 1000, 1024, 7, 700]
+    sk, sv = dev(_rand_bits(rng, (S, Hkv, D))), dev(_rand_bits(rng, (S, Hkv, D)))
+    ring0 = _rand_bits(rng, (R, Hkv, D))
+    rk_a, rv_a = dev(ring0), dev(ring0.copy())
+    rk_b, rv_b = dev(ring0.copy()), dev(ring0.copy())
+    mk, mv = oracle.RingModel(R, (Hkv, D)), oracle.RingModel(R, (Hkv, D))
+    mk.buf[:] = ring0
+    mv.buf[:] = ring0
+    ws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    H = 5 * R + 333
+    for c in counts:
+        qb, kb, vb = (_rand_bits(rng, (c, Hq, D)), _rand_bits(rng, (c, Hkv, D)), _rand_bits(rng, (c, Hkv, D)))
+        q, k, v = dev(qb), dev(kb), dev(vb)
+        outs = []
+        for rk, rv, fl in ((rk_a, rv_a, flags), (rk_b, rv_b, flags | vico.VICO_ATTN_APPEND)):
+            out = torch.empty((c, Hq, D), dtype=torch.float32, device="cuda")
+            lse = torch.empty((Hq, c), dtype=torch.float32, device="cuda")
+            assert vico.vico_attn_plan(c, S, R, H, W, Hq, Hkv, D, splits, fl)[1] <= ws.numel()
+            vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, H, W, out, lse=lse, workspace=ws,
+                                         num_splits=splits, flags=fl)
+            if not fl & vico.VICO_ATTN_APPEND:
+                vico.vico_kv_append(k, v, rk, rv, H)
+            outs.append((out, lse))
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+        assert torch.equal(rk_a, rk_b) and torch.equal(rv_a, rv_b)
+        mk.append(kb, H)
+        mv.append(vb, H)
+        assert np.array_equal(bits_of(rk_b), mk.buf) and np.array_equal(bits_of(rv_b), mv.buf)
+        H += c
