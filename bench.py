@@ -41,7 +41,8 @@ KERNEL_SRC = {"attn_fwd_kernel<128>": [CSRC + "attn_fwd.hip", CSRC + "attn_commo
               "attn_gather_kernel<128>": [CSRC + "attn_gather.hip", CSRC + "attn_merge.hip", CSRC + "attn_common.h",
                                           CSRC + "vico_internal.h"],
               "kv_append_kernel": [CSRC + "kv_append.hip"],
-              "drop_sim_kernel<4>": [CSRC + "token_drop.hip"]}
+              "drop_sim_kernel<4>": [CSRC + "token_drop.hip", CSRC + "token_drop.h"],
+              "drop_fused_kernel<4, 7>": [CSRC + "token_drop.hip", CSRC + "token_drop.h"]}
 
 
 def kernel_source_sha256(kernel):
@@ -589,7 +590,8 @@ def run_query_workload(args, torch, vico):
 def run_drop_workload(args, torch, vico):
     """Temporal token dropping of a batch of chunks (HBM bound): algorithmic
     bytes = the frames read once + the retained tokens and their indices
-    written once."""
+    written once.  --drop-schedule picks the single pass (a workspace given,
+    the default) or the two passes (none)."""
     from synth import make_drop_frames
     B, C, n_f, dm, tau = 16, 4, 256, 3584, 0.9
     n_batches = 4
@@ -598,15 +600,24 @@ def run_drop_workload(args, torch, vico):
     idx = torch.empty(B * C * n_f, dtype=torch.int32, device="cuda")
     cnt = torch.empty(1, dtype=torch.int32, device="cuda")
     out = torch.empty((B * C * n_f, dm), dtype=torch.bfloat16, device="cuda")
+    single = args.drop_schedule == "single_pass"
+    ws = None
+    if single:
+        nb = vico.vico_temporal_drop_workspace_bytes(B, C, n_f, dm)
+        ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+
+    def call(fr):
+        vico.vico_temporal_drop(fr, tau, keep, idx, cnt, out_tokens=out, workspace=ws, stream=stream)
+
     kept = []
     for fr in batches:
-        vico.vico_temporal_drop(fr, tau, keep, idx, cnt, out_tokens=out, stream=stream)
+        call(fr)
         torch.cuda.synchronize()
         kept.append(int(cnt.item()))
-    n_warm = warm_up(torch, lambda j: vico.vico_temporal_drop(batches[j % n_batches], tau, keep, idx, cnt,
-                                                              out_tokens=out, stream=stream),
-                     args.warmup, args.warmup_seconds)
+        if kept[-1] < 0:
+            raise RuntimeError("temporal drop: a bounded wait of the single pass gave up")
+    n_warm = warm_up(torch, lambda j: call(batches[j % n_batches]), args.warmup, args.warmup_seconds)
     busy = Busy(torch)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -614,10 +625,11 @@ def run_drop_workload(args, torch, vico):
     busy.hold(stream)
     for j in range(args.steps):
         ev[j][0].record(stream)
-        vico.vico_temporal_drop(batches[(n_warm + j) % n_batches], tau, keep, idx, cnt, out_tokens=out,
-                                stream=stream)
+        call(batches[(n_warm + j) % n_batches])
         ev[j][1].record(stream)
     torch.cuda.synchronize()
+    if int(cnt.item()) != kept[(n_warm + args.steps - 1) % n_batches]:
+        raise RuntimeError("temporal drop: the last timed call retained a different count")
     host_paced = B * C * n_f * args.steps / (time.perf_counter() - t0)
     elapsed = ev[0][0].elapsed_time(ev[-1][1]) * 1e-3          # GPU span of the calls, fed ahead
     ms = np.array([a.elapsed_time(b) for a, b in ev])
@@ -625,18 +637,21 @@ def run_drop_workload(args, torch, vico):
     in_bytes = B * C * n_f * dm * 2
     alg = in_bytes + n_keep * (dm * 2 + 4) + B * n_f
     gbs = float(np.mean(alg / (ms * 1e-3)) / 1e9)
+    kernel = "drop_fused_kernel<4, 7>" if single else "drop_sim_kernel<4>"
     return {
         "metric": "temporal token dropping throughput (input tokens/s)",
         "value": round(B * C * n_f * args.steps / elapsed, 1), "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": DESCR["drop"], "retention": round(float(n_keep.mean()) / (B * C * n_f), 4)},
+        "config": {"workload": DESCR["drop"], "retention": round(float(n_keep.mean()) / (B * C * n_f), 4),
+                   "schedule": args.drop_schedule},
         "call_us_mean": round(float(ms.mean()) * 1e3, 2),
         "host_paced_tokens_per_s": round(host_paced, 1),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "traffic": measured_traffic("drop_sim_kernel<4>", "drop"),
-                     "kernel": "drop_sim_kernel<4> + drop_compact_kernel",
+                     "traffic": measured_traffic(kernel, "drop" if single else "drop_two_pass"),
+                     "kernel": ("drop_reset_kernel + drop_fused_kernel<4, 7>" if single
+                                else "drop_sim_kernel<4> + drop_compact_kernel"),
                      "bytes_per_launch_mean": float(alg.mean())},
     }
 
@@ -694,6 +709,8 @@ def main():
     ap.add_argument("--workload", default="7b", choices=["7b", "3b", "full", "full_bounded", "stream", "append", "query", "decode",
                                                           "drop"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--drop-schedule", default="single_pass", choices=["single_pass", "two_pass"],
+                    help="drop workload: single pass (workspace given) or two passes")
     ap.add_argument("--only-variant", default=None,
                     help="chunk workloads: time only this variant (e.g. warm_wrapped), for profiling runs")
     ap.add_argument("--ramp", action="store_true",

@@ -349,12 +349,42 @@ int vico_gather_attn_noalloc(const void* q, int32_t q_len, const void* tail_k, c
  *               (chunk*C + frame)*tokens_per_frame + position of each
  *               retained token, in the same order
  *   out_count   [1] int32: number of retained tokens
+ *   workspace   NULL, or device scratch of at least
+ *               vico_temporal_drop_workspace_bytes(...) bytes, 8-byte aligned,
+ *               overlapping no other argument (VICO_ERR_WORKSPACE if smaller,
+ *               VICO_ERR_MISALIGNED if not aligned); its contents need no
+ *               initialisation and are meaningless afterwards.  Calls that share
+ *               one workspace must be ordered (same stream, or synchronised).
  * 1 <= C <= 8, feat_dim a positive multiple of 8, fewer than 2^31 rows;
- * num_chunks == 0 is a no-op.  Two kernels, no workspace.
+ * num_chunks == 0 is a no-op.
+ *
+ * Schedules (same results, bit for bit):
+ *   workspace NULL, or a shape the single pass does not cover (workspace
+ *   bytes 0): two passes -- similarities and flags, then ranking and copying,
+ *   which reads the retained rows a second time.
+ *   otherwise: one pass in which each token row is read once and stored at
+ *   its final place; its work-groups share their counts of kept positions
+ *   through the workspace (words tagged per call, so no zeroing is needed).
+ *   A work-group that waits more than 200 us for another one's count
+ *   (environment variable VICO_DROP_WAIT_US, read at every call) recomputes it from
+ *   the frames instead, so the results never depend on scheduling.
  */
 int vico_temporal_drop(const void* frames, int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
                        int32_t feat_dim, float tau, const void* prev_frame, uint8_t* keep, float* sim,
-                       void* out_tokens, int32_t* out_index, int32_t* out_count, void* stream);
+                       void* out_tokens, int32_t* out_index, int32_t* out_count, void* workspace,
+                       int64_t workspace_bytes, void* stream);
+
+/*
+ * vico_temporal_drop_workspace_bytes -- workspace bytes of the single-pass
+ * schedule of vico_temporal_drop for these sizes: 0 where that schedule does
+ * not apply (num_chunks == 0 or above 256, tokens_per_frame > 1024, or
+ * feat_dim above 512 * min(8, 32 / max(C, 2)) with integer division: 4096 up
+ * to C = 4, then 3072, 2560, 2048, 2048), VICO_ERR_INVALID_ARG for sizes
+ * vico_temporal_drop rejects.  128 bytes per chunk and 8 per tile of 4
+ * positions: num_chunks * (128 + 8 * ceil(tokens_per_frame / 4)).
+ */
+int64_t vico_temporal_drop_workspace_bytes(int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
+                                           int32_t feat_dim);
 
 /* Static text for a vico_status value. */
 const char* vico_status_str(int status);

@@ -34,6 +34,7 @@ from ._binding import (
     vico_gather_attn_noalloc,
     vico_acn_window,
     vico_temporal_drop,
+    vico_temporal_drop_workspace_bytes,
 )
 
 __all__ = [
@@ -59,4 +60,5 @@ __all__ = [
     "vico_gather_attn_noalloc",
     "vico_acn_window",
     "vico_temporal_drop",
+    "vico_temporal_drop_workspace_bytes",
 ]

@@ -39,7 +39,8 @@ _SIGNATURES = {
     "vico_attn_plan_ex": (_i32, [_i32, _i32, _i32, _i64, _i64, _i32, _i32, _i32, _i32, _i32,
                                  ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "vico_acn_window": (_i64, [ctypes.POINTER(_i64), _i32, _i32, _i32]),
-    "vico_temporal_drop": (_i32, [_vp, _i32, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "vico_temporal_drop": (_i32, [_vp, _i32, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp]),
+    "vico_temporal_drop_workspace_bytes": (_i64, [_i32, _i32, _i32, _i32]),
     "vico_token_mean": (_i32, [_vp, _i32, _i32, _vp, _vp]),
     "vico_chunk_scores": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "vico_topk_chunks": (_i32, [_vp, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -289,9 +290,20 @@ def vico_gather_attn_noalloc(q, tail_k, tail_v, sink_k, sink_v, store_k, store_v
     _check(st, "vico_gather_attn_noalloc")
 
 
+def vico_temporal_drop_workspace_bytes(num_chunks: int, frames_per_chunk: int, tokens_per_frame: int,
+                                       feat_dim: int) -> int:
+    """Workspace bytes of the single-pass drop (0: that schedule does not apply)."""
+    b = load_library().vico_temporal_drop_workspace_bytes(num_chunks, frames_per_chunk, tokens_per_frame, feat_dim)
+    if b < 0:
+        raise VicoError(int(b), "vico_temporal_drop_workspace_bytes")
+    return int(b)
+
+
 def vico_temporal_drop(frames, tau: float, keep, out_index, out_count, sim=None, out_tokens=None, prev_frame=None,
-                       stream=None) -> None:
-    """Chunk-level temporal token dropping (vico_temporal_drop); frames bf16 [B, C, n_f, dm]."""
+                       workspace=None, stream=None) -> None:
+    """Chunk-level temporal token dropping (vico_temporal_drop); frames bf16 [B, C, n_f, dm].
+    With a workspace of vico_temporal_drop_workspace_bytes(B, C, n_f, dm) bytes
+    the call takes the single-pass schedule where it applies."""
     _dev_tensor("frames", frames, torch.bfloat16, 4)
     B, C, n_f, dm = frames.shape
     _dev_tensor("keep", keep, torch.uint8, 2)
@@ -309,7 +321,10 @@ def vico_temporal_drop(frames, tau: float, keep, out_index, out_count, sim=None,
             raise ValueError("out_tokens must hold B*C*n_f rows of dm")
     if prev_frame is not None:
         _dev_tensor("prev_frame", prev_frame, torch.bfloat16, 2)
+    if workspace is not None and (not workspace.is_cuda or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous device tensor")
+    wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = load_library().vico_temporal_drop(_ptr(frames), B, C, n_f, dm, float(tau), _ptr(prev_frame), _ptr(keep),
                                            _ptr(sim), _ptr(out_tokens), _ptr(out_index), _ptr(out_count),
-                                           _stream(stream))
+                                           _ptr(workspace), wb, _stream(stream))
     _check(st, "vico_temporal_drop")

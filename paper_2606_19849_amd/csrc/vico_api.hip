@@ -9,6 +9,7 @@
 
 #include "vico.h"
 #include "vico_internal.h"
+#include "token_drop.h"
 
 namespace {
 
@@ -177,6 +178,13 @@ bool aligned_to(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t
 int hip_fail(hipError_t e) {
   g_last_hip_error = (int)e;
   return VICO_ERR_HIP;
+}
+
+bool drop_shape_ok(int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame, int32_t feat_dim) {
+  if (num_chunks < 0 || frames_per_chunk < 1 || frames_per_chunk > 8 || tokens_per_frame < 1 || feat_dim < 8 ||
+      feat_dim % 8 != 0)
+    return false;
+  return int64_t(num_chunks) * frames_per_chunk * tokens_per_frame < (int64_t(1) << 31);
 }
 
 }  // namespace
@@ -511,30 +519,40 @@ int vico::gather_attn_entry(const void* q, int32_t q_len, const void* tail_k, co
 
 extern "C" {
 
+int64_t vico_temporal_drop_workspace_bytes(int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
+                                           int32_t feat_dim) {
+  if (!drop_shape_ok(num_chunks, frames_per_chunk, tokens_per_frame, feat_dim)) return VICO_ERR_INVALID_ARG;
+  return vico::temporal_drop_workspace_bytes(num_chunks, frames_per_chunk, tokens_per_frame, feat_dim);
+}
+
 int vico_temporal_drop(const void* frames, int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
                        int32_t feat_dim, float tau, const void* prev_frame, uint8_t* keep, float* sim,
-                       void* out_tokens, int32_t* out_index, int32_t* out_count, void* stream) {
-  if (num_chunks < 0 || frames_per_chunk < 1 || frames_per_chunk > 8 || tokens_per_frame < 1 || feat_dim < 8 ||
-      feat_dim % 8 != 0 || isnan(tau))
+                       void* out_tokens, int32_t* out_index, int32_t* out_count, void* workspace,
+                       int64_t workspace_bytes, void* stream) {
+  if (!drop_shape_ok(num_chunks, frames_per_chunk, tokens_per_frame, feat_dim) || isnan(tau) || workspace_bytes < 0)
     return VICO_ERR_INVALID_ARG;
   const int64_t rows = int64_t(num_chunks) * frames_per_chunk * tokens_per_frame;
-  if (rows >= (int64_t(1) << 31)) return VICO_ERR_INVALID_ARG;
   if (num_chunks == 0) return VICO_OK;
   if (!frames || !keep || !out_index || !out_count) return VICO_ERR_INVALID_ARG;
+  const int64_t need = workspace ? vico::temporal_drop_workspace_bytes(num_chunks, frames_per_chunk, tokens_per_frame,
+                                                                       feat_dim) : 0;
   if (!aligned16(frames) || (prev_frame && !aligned16(prev_frame)) || (out_tokens && !aligned16(out_tokens)) ||
-      !aligned_to(sim, 4) || !aligned_to(out_index, 4) || !aligned_to(out_count, 4))
+      !aligned_to(sim, 4) || !aligned_to(out_index, 4) || !aligned_to(out_count, 4) ||
+      (need && !aligned_to(workspace, 8)))
     return VICO_ERR_MISALIGNED;
   const int64_t fb = rows * feat_dim * 2, pb = prev_frame ? int64_t(tokens_per_frame) * feat_dim * 2 : 0;
   const int64_t kb = int64_t(num_chunks) * tokens_per_frame;
-  const void* outs[] = {keep, sim, out_tokens, out_index, out_count};
-  const int64_t outb[] = {kb, sim ? kb * 4 : 0, out_tokens ? fb : 0, rows * 4, 4};
-  for (int i = 0; i < 5; ++i) {
+  const void* outs[] = {keep, sim, out_tokens, out_index, out_count, need ? workspace : nullptr};
+  const int64_t outb[] = {kb, sim ? kb * 4 : 0, out_tokens ? fb : 0, rows * 4, 4, need};
+  for (int i = 0; i < 6; ++i) {
     if (!outs[i]) continue;
     if (overlaps(outs[i], outb[i], frames, fb) || overlaps(outs[i], outb[i], prev_frame, pb)) return VICO_ERR_INVALID_ARG;
-    for (int j = i + 1; j < 5; ++j)
+    for (int j = i + 1; j < 6; ++j)
       if (outs[j] && overlaps(outs[i], outb[i], outs[j], outb[j])) return VICO_ERR_INVALID_ARG;
   }
+  if (need && workspace_bytes < need) return VICO_ERR_WORKSPACE;
   vico::DropArgs a{};
+  a.ws = need ? workspace : nullptr;
   a.frames = (const uint16_t*)frames;
   a.prev = frames_per_chunk == 1 ? (const uint16_t*)prev_frame : nullptr;
   a.keep = keep;

@@ -74,19 +74,6 @@ struct GatherArgs {
   float scale_log2;
 };
 
-// Temporal token dropping over B chunks of C frames of n_f tokens of dm features.
-struct DropArgs {
-  const uint16_t* frames;   // [B][C][n_f][dm] bf16
-  const uint16_t* prev;     // [n_f][dm] frame before the batch (C == 1), may be null
-  uint8_t* keep;            // [B][n_f] 1 = position kept
-  float* sim;               // [B][n_f] smallest pairwise cosine, may be null
-  uint16_t* out;            // [B*C*n_f][dm] retained tokens in stream order, may be null
-  int32_t* out_index;       // [B*C*n_f] flat source row of each retained token
-  int32_t* out_count;       // [1]
-  int B, C, n_f, dm;
-  float tau;
-};
-
 struct AppendArgs {
   const uint16_t* kc;
   const uint16_t* vc;
@@ -122,7 +109,6 @@ hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream);
 hipError_t launch_merge(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
-hipError_t launch_temporal_drop(const DropArgs& a, hipStream_t stream);
 // Records e as the calling thread's last HIP error; returns VICO_ERR_HIP.
 int record_hip_failure(hipError_t e);
 

@@ -16,7 +16,8 @@ MIS = 0x10008
 EXPECTED = {"vico_kv_append", "vico_chunk_prefill_attn", "vico_attn_plan", "vico_attn_workspace_bytes",
             "vico_status_str", "vico_last_hip_error", "vico_token_mean", "vico_chunk_scores", "vico_topk_chunks",
             "vico_gather_plan", "vico_gather_attn", "vico_chunk_prefill_attn_ex", "vico_attn_plan_ex",
-            "vico_acn_window", "vico_temporal_drop", "vico_gather_attn_noalloc"}
+            "vico_acn_window", "vico_temporal_drop", "vico_gather_attn_noalloc",
+            "vico_temporal_drop_workspace_bytes"}
 
 
 def test_header_declares_the_expected_entry_points():
@@ -386,10 +387,10 @@ def test_balanced_plan_counts_whole_chunks_when_bidirectional():
 
 def _drop(**kw):
     a = dict(fr=A, B=2, C=4, nf=24, dm=64, tau=0.9, prev=None, keep=B, sim=B + 0x1000, out=B + 0x10000,
-             idx=B + 0x100000, cnt=B + 0x200000)
+             idx=B + 0x100000, cnt=B + 0x200000, ws=None, wsb=0)
     a.update(kw)
     return lib.vico_temporal_drop(a["fr"], a["B"], a["C"], a["nf"], a["dm"], a["tau"], a["prev"], a["keep"],
-                                  a["sim"], a["out"], a["idx"], a["cnt"], None)
+                                  a["sim"], a["out"], a["idx"], a["cnt"], a["ws"], a["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -398,6 +399,11 @@ def _drop(**kw):
     (dict(cnt=None), -1), (dict(fr=MIS), -4), (dict(out=B + 0x10008), -4), (dict(idx=B + 0x100002), -4),
     (dict(keep=A + 0x100), -1),              # keep inside the frames
     (dict(out=B + 0x800), -1),               # out_tokens over sim
+    (dict(ws=B + 0x300000, wsb=-8), -1),
+    (dict(ws=B + 0x300000, wsb=351), -5),    # one byte short of the 352 the shape needs
+    (dict(ws=B + 0x300004, wsb=4096), -4),   # control words are 8-byte aligned
+    (dict(ws=B + 0x10, wsb=4096), -1),       # workspace over keep (48 bytes)
+    (dict(ws=A + 0x40, wsb=4096), -1),       # workspace inside the frames
 ])
 def test_temporal_drop_rejects_bad_arguments(kw, status):
     assert _drop(**kw) == status
@@ -405,6 +411,33 @@ def test_temporal_drop_rejects_bad_arguments(kw, status):
 
 def test_temporal_drop_of_no_chunks_is_a_no_op():
     assert _drop(B=0) == 0
+    assert _drop(B=0, ws=B + 0x300000, wsb=0) == 0
+
+
+def _ws(B, n_f):
+    """A 128-byte line per chunk and an 8-byte word per tile of 4 positions."""
+    return 128 * B + 8 * B * -(-n_f // 4)
+
+
+@pytest.mark.parametrize("shape,want", [
+    ((2, 4, 24, 64), _ws(2, 24)),
+    ((16, 4, 256, 3584), _ws(16, 256)),
+    ((3, 1, 40, 4096), _ws(3, 40)),          # C = 1 compares 2 rows: 8 units of 512 features fit
+    ((3, 1, 40, 4104), 0),                   # 9 units per lane: two passes
+    ((3, 4, 41, 4096), _ws(3, 41)),
+    ((3, 5, 40, 3072), _ws(3, 40)),
+    ((3, 5, 40, 3080), 0),
+    ((3, 8, 40, 2048), _ws(3, 40)),
+    ((3, 8, 40, 2056), 0),
+    ((3, 4, 1024, 64), _ws(3, 1024)),
+    ((3, 4, 1025, 64), 0),                   # more than 256 tiles per chunk
+    ((256, 4, 24, 64), _ws(256, 24)),        # the most chunks one call takes
+    ((257, 4, 24, 64), 0),
+    ((0, 4, 24, 64), 0),
+    ((2, 9, 24, 64), -1), ((2, 4, 24, 60), -1), ((-1, 4, 24, 64), -1), ((1 << 20, 8, 1 << 10, 8), -1),
+])
+def test_temporal_drop_workspace_bytes(shape, want):
+    assert lib.vico_temporal_drop_workspace_bytes(*shape) == want
 
 
 # ---- measurement helper library (libvico_bench.so, include/vico_bench.h)

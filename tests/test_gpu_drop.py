@@ -25,8 +25,23 @@ f64 = oracle.bf16_bits_to_f64
 U = 2.0 ** -24
 
 
-def run_gpu(frames_bits, tau, prev_bits=None, with_tokens=True):
+SCHEDULES = ["two_pass", "single_pass"]
+
+
+def workspace_for(shape, schedule, fill=0xFF):
+    """The workspace that selects `schedule` (None: two passes); filled with
+    garbage, since the call must not rely on its contents."""
+    if schedule == "two_pass":
+        return None
+    nb = vico.vico_temporal_drop_workspace_bytes(*shape)
+    assert nb > 0, f"{shape}: the single pass should apply"
+    return torch.full((nb,), fill, dtype=torch.uint8, device="cuda")
+
+
+def run_gpu(frames_bits, tau, prev_bits=None, with_tokens=True, schedule="two_pass", workspace=None):
     B, C, n_f, dm = frames_bits.shape
+    if workspace is None:
+        workspace = workspace_for(frames_bits.shape, schedule)
     fr = dev(frames_bits)
     keep = torch.full((B, n_f), 7, dtype=torch.uint8, device="cuda")
     sim = torch.full((B, n_f), float("nan"), dtype=torch.float32, device="cuda")
@@ -34,16 +49,16 @@ def run_gpu(frames_bits, tau, prev_bits=None, with_tokens=True):
     cnt = torch.full((1,), -1, dtype=torch.int32, device="cuda")
     out = torch.zeros((B * C * n_f, dm), dtype=torch.bfloat16, device="cuda") if with_tokens else None
     prev = dev(prev_bits) if prev_bits is not None else None
-    vico.vico_temporal_drop(fr, tau, keep, idx, cnt, sim=sim, out_tokens=out, prev_frame=prev)
+    vico.vico_temporal_drop(fr, tau, keep, idx, cnt, sim=sim, out_tokens=out, prev_frame=prev, workspace=workspace)
     torch.cuda.synchronize()
     n = int(cnt.item())
     return dict(keep=keep.cpu().numpy(), sim=sim.cpu().numpy(), idx=idx.cpu().numpy(), n=n,
                 out=bits_of(out[:n]) if with_tokens else None)
 
 
-def check(frames_bits, tau, prev_bits=None, with_tokens=True):
+def check(frames_bits, tau, prev_bits=None, with_tokens=True, schedule="two_pass"):
     B, C, n_f, dm = frames_bits.shape
-    g = run_gpu(frames_bits, tau, prev_bits, with_tokens)
+    g = run_gpu(frames_bits, tau, prev_bits, with_tokens, schedule)
     z = f64(frames_bits)
     keep_ref, sim_ref, _ = oracle.temporal_drop(z, tau, None if prev_bits is None else f64(prev_bits))
     bound = (3 * dm + 8) * U
@@ -64,56 +79,133 @@ def check(frames_bits, tau, prev_bits=None, with_tokens=True):
     return g, keep_ref
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("name", ["tiny", "c2", "c8", "7b", "3b"])
 @pytest.mark.parametrize("tau", [0.9, 0.5])
-def test_drop_parity(name, tau):
+def test_drop_parity(name, tau, schedule):
     B, C, n_f, dm = DROP_CONFIGS[name]
-    g, keep_ref = check(make_drop_frames(B, C, n_f, dm, seed=B + C + n_f), tau)
+    g, keep_ref = check(make_drop_frames(B, C, n_f, dm, seed=B + C + n_f), tau, schedule=schedule)
     assert 0 < g["keep"].mean() < 1                 # both outcomes occur
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("with_prev", [False, True])
-def test_frame_level_mode(with_prev):
+def test_frame_level_mode(with_prev, schedule):
     B, C, n_f, dm = DROP_CONFIGS["c1"]
     frames = make_drop_frames(B, C, n_f, dm, seed=11)
     prev = make_drop_frames(1, 1, n_f, dm, seed=11)[0, 0] if with_prev else None
-    check(frames, 0.8, prev)
+    check(frames, 0.8, prev, schedule=schedule)
 
 
-def test_indices_only():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_indices_only(schedule):
     B, C, n_f, dm = DROP_CONFIGS["tiny"]
-    check(make_drop_frames(B, C, n_f, dm, seed=12), 0.9, with_tokens=False)
+    check(make_drop_frames(B, C, n_f, dm, seed=12), 0.9, with_tokens=False, schedule=schedule)
 
 
-def test_identical_frames_keep_only_anchors():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_identical_frames_keep_only_anchors(schedule):
     base = make_drop_frames(3, 1, 40, 128, seed=13)
     frames = np.repeat(base, 4, axis=1)
-    g, _ = check(frames, 0.5)
+    g, _ = check(frames, 0.5, schedule=schedule)
     assert not g["keep"].any() and g["n"] == 3 * 40
 
 
-def test_exact_cosine_at_the_threshold_is_kept():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_exact_cosine_at_the_threshold_is_kept(schedule):
     """(3, 4) and (4, 3) have cosine 24/25: exact in fp32 (norms 5, dot 24),
     so tau = 0.96 (as fp32) must not drop, and any smaller tau must."""
     frames = np.zeros((1, 2, 4, 64), dtype=np.float32)
     frames[0, 0, :, :2] = (3, 4)
     frames[0, 1, :, :2] = (4, 3)
     bits = frames.view(np.uint32).__rshift__(16).astype(np.uint16)       # exact: small integers
-    g = run_gpu(bits, float(np.float32(0.96)))
+    g = run_gpu(bits, float(np.float32(0.96)), schedule=schedule)
     assert np.all(g["sim"] == np.float32(0.96)) and g["keep"].all()
-    g = run_gpu(bits, float(np.nextafter(np.float32(0.96), np.float32(0))))
+    g = run_gpu(bits, float(np.nextafter(np.float32(0.96), np.float32(0))), schedule=schedule)
     assert not g["keep"].any()
 
 
-def test_zero_vectors_score_zero():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_zero_vectors_score_zero(schedule):
     frames = np.zeros((2, 3, 8, 32), dtype=np.uint16)
     frames[:, :, 4:, 0] = 0x3F80                                        # 1.0 at the last four positions
-    g = run_gpu(frames, -0.5)
+    g = run_gpu(frames, -0.5, schedule=schedule)
     assert np.all(g["sim"][:, :4] == 0) and np.all(g["sim"][:, 4:] == 1) and not g["keep"].any()
 
 
-def test_many_chunks_ranks_across_chunks():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_many_chunks_ranks_across_chunks(schedule):
     """64 chunks of the 3B shape at tau 0.9: output offsets of each chunk depend
     on the counts of all earlier chunks."""
     frames = make_drop_frames(64, 4, 64, 256, seed=14)
-    check(frames, 0.9)
+    check(frames, 0.9, schedule=schedule)
+
+
+@pytest.mark.parametrize("shape,tau,with_prev", [
+    ((150, 2, 40, 128), 0.9, False),     # the look-back spans three windows of 64 chunks
+    ((5, 1, 1024, 64), 0.8, True),       # 256 tiles per chunk, the most the single pass takes
+    ((7, 3, 37, 4096), 0.9, False),      # 8 units of 512 features per lane, ragged tiles
+    ((4, 8, 50, 2048), 0.5, False),      # C = 8 at its widest single-pass row
+    ((9, 1, 13, 200), 0.8, False),       # C = 1 without a previous frame; 25 pieces of a row
+])
+def test_schedules_agree_bit_for_bit(shape, tau, with_prev):
+    """Both schedules run the same arithmetic: every output is the same bits,
+    and the single pass meets the oracle on its own."""
+    B, C, n_f, dm = shape
+    frames = make_drop_frames(B, C, n_f, dm, seed=B * 31 + C)
+    prev = make_drop_frames(1, 1, n_f, dm, seed=B * 31 + C + 1)[0, 0] if with_prev else None
+    one, _ = check(frames, tau, prev, schedule="single_pass")
+    two = run_gpu(frames, tau, prev, schedule="two_pass")
+    assert one["n"] == two["n"]
+    for k in ("keep", "idx", "out"):
+        assert np.array_equal(one[k], two[k]), k
+    assert np.array_equal(one["sim"].view(np.uint32), two["sim"].view(np.uint32))
+
+
+@pytest.mark.parametrize("shape,tau,with_prev", [
+    ((5, 4, 24, 256), 0.9, False),
+    ((4, 1, 13, 200), 0.8, True),
+    ((3, 1, 9, 64), 0.8, False),
+    ((70, 2, 8, 64), 0.9, False),        # chunk counts beyond one window of 64
+])
+def test_single_pass_recount_path(monkeypatch, shape, tau, with_prev):
+    """With no time to wait, every group recounts what it needs from the
+    frames: the results are still those of the two passes, bit for bit."""
+    B, C, n_f, dm = shape
+    frames = make_drop_frames(B, C, n_f, dm, seed=B * 7 + C)
+    prev = make_drop_frames(1, 1, n_f, dm, seed=B * 7 + C + 1)[0, 0] if with_prev else None
+    two = run_gpu(frames, tau, prev, schedule="two_pass")
+    monkeypatch.setenv("VICO_DROP_WAIT_US", "0")
+    one = run_gpu(frames, tau, prev, schedule="single_pass")
+    assert one["n"] == two["n"]
+    for k in ("keep", "idx", "out"):
+        assert np.array_equal(one[k], two[k]), k
+    assert np.array_equal(one["sim"].view(np.uint32), two["sim"].view(np.uint32))
+
+
+def test_single_pass_workspace_reuse():
+    """One workspace across calls of different sizes, on one stream: each call
+    starts from its own zeroed control block."""
+    big = make_drop_frames(16, 4, 96, 512, seed=21)
+    small = make_drop_frames(3, 4, 40, 512, seed=22)
+    ws = workspace_for(big.shape, "single_pass")
+    for frames in (big, small, big):
+        one = run_gpu(frames, 0.9, schedule="single_pass", workspace=ws)
+        two = run_gpu(frames, 0.9, schedule="two_pass")
+        assert one["n"] == two["n"] and one["n"] > 0
+        for k in ("keep", "idx", "out"):
+            assert np.array_equal(one[k], two[k]), k
+
+
+def test_single_pass_not_covered_runs_two_passes():
+    """A workspace with a shape the single pass does not take is ignored."""
+    B, C, n_f, dm = 2, 8, 24, 2056
+    assert vico.vico_temporal_drop_workspace_bytes(B, C, n_f, dm) == 0
+    ws = torch.full((256,), 0xFF, dtype=torch.uint8, device="cuda")
+    frames = make_drop_frames(B, C, n_f, dm, seed=23)
+    two, _ = check(frames, 0.5, schedule="two_pass")
+    given = run_gpu(frames, 0.5, workspace=ws)
+    assert given["n"] == two["n"]
+    for k in ("keep", "idx", "out"):
+        assert np.array_equal(given[k], two[k]), k
+    assert torch.all(ws == 0xFF)                     # untouched
