@@ -650,8 +650,7 @@ def run_drop_workload(args, torch, vico):
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "traffic": measured_traffic(kernel, "drop" if single else "drop_two_pass"),
-                     "kernel": ("drop_reset_kernel + drop_fused_kernel<4, 7>" if single
-                                else "drop_sim_kernel<4> + drop_compact_kernel"),
+                     "kernel": "drop_fused_kernel<4, 7>" if single else "drop_sim_kernel<4> + drop_compact_kernel",
                      "bytes_per_launch_mean": float(alg.mean())},
     }
 
