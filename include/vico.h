@@ -367,7 +367,9 @@ int vico_gather_attn_noalloc(const void* q, int32_t q_len, const void* tail_k, c
  *   through the workspace (words tagged per call, so no zeroing is needed).
  *   A work-group that waits more than 200 us for another one's count
  *   (environment variable VICO_DROP_WAIT_US, read at every call) recomputes it from
- *   the frames instead, so the results never depend on scheduling.
+ *   the frames instead, so the results never depend on scheduling.  Under
+ *   HIP graph capture the call takes the two passes (the single pass tags its
+ *   words per call, and a replayed graph would repeat the tag).
  */
 int vico_temporal_drop(const void* frames, int32_t num_chunks, int32_t frames_per_chunk, int32_t tokens_per_frame,
                        int32_t feat_dim, float tau, const void* prev_frame, uint8_t* keep, float* sim,

@@ -700,7 +700,14 @@ int64_t temporal_drop_workspace_bytes(int B, int C, int n_f, int dm) {
 
 hipError_t launch_temporal_drop(const DropArgs& a, hipStream_t stream) {
   const int64_t items = (int64_t)a.B * a.n_f;
-  if (a.ws) {                                   // single pass
+  // single pass, except under graph capture: a replayed graph would repeat
+  // the call's epoch and read the words of the previous replay as its own
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  if (a.ws && hipStreamIsCapturing(stream, &capture) != hipSuccess) {
+    (void)hipGetLastError();
+    capture = hipStreamCaptureStatusActive;       // unknown: take the two passes
+  }
+  if (a.ws && capture == hipStreamCaptureStatusNone) {
     const FusedFn fn = fused_kernel_for(a.B, a.C, a.n_f, a.dm);
     if (!fn) return hipErrorInvalidValue;
     DropArgs args = a;

@@ -209,3 +209,47 @@ def test_single_pass_not_covered_runs_two_passes():
     for k in ("keep", "idx", "out"):
         assert np.array_equal(given[k], two[k]), k
     assert torch.all(ws == 0xFF)                     # untouched
+
+
+def test_drop_with_workspace_replays_as_a_graph():
+    """Captured into a HIP graph, a call with a workspace takes the two passes
+    (the single pass tags its words per call, which replays would repeat): the
+    replays reproduce the eager result, with eager single-pass calls on other
+    inputs and the same buffers in between."""
+    B, C, n_f, dm = 6, 4, 40, 512
+    frames = [dev(make_drop_frames(B, C, n_f, dm, seed=31 + i)) for i in range(2)]
+    ws = workspace_for((B, C, n_f, dm), "single_pass")
+    keep = torch.empty((B, n_f), dtype=torch.uint8, device="cuda")
+    idx = torch.empty(B * C * n_f, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    out = torch.empty((B * C * n_f, dm), dtype=torch.bfloat16, device="cuda")
+
+    def step(i):
+        vico.vico_temporal_drop(frames[i], 0.9, keep, idx, cnt, out_tokens=out, workspace=ws)
+
+    eager = []
+    for i in range(2):
+        step(i)
+        torch.cuda.synchronize()
+        n = int(cnt.item())
+        eager.append((keep.clone(), idx[:n].clone(), out[:n].clone(), n))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        step(0)
+        torch.cuda.current_stream().synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            step(0)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        step(1)
+        torch.cuda.synchronize()
+        k, i1, o, n = eager[1]
+        assert int(cnt.item()) == n and torch.equal(keep, k) and torch.equal(idx[:n], i1) and torch.equal(out[:n], o)
+        keep.fill_(7)
+        idx.fill_(-5)
+        graph.replay()
+        torch.cuda.synchronize()
+        k, i0, o, n = eager[0]
+        assert int(cnt.item()) == n and torch.equal(keep, k) and torch.equal(idx[:n], i0) and torch.equal(out[:n], o)
