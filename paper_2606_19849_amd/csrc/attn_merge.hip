@@ -23,6 +23,7 @@ namespace {
 
 constexpr int kMergeThreads = 256;
 constexpr int kFewParts = 8;     // up to here one thread per (row, 4 columns) loads all parts
+constexpr int kPartsPerThread = 8;   // many parts: parts one thread loads (64 parts over 8 part groups)
 
 // With an append requested, the blocks past `merge_blocks` copy the chunk's
 // K/V into the ring instead of merging: this launch runs after every read of
@@ -124,11 +125,24 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a, i
   const int64_t hr = r0 + r;
   f32x4 acc{0.f, 0.f, 0.f, 0.f};
   if (r < RPB && hr < n_rows) {
-    for (int p = pg; p < a.splits; p += PG) {
-      const float w = w_s[r][p];
-      const f32x4 v = *(const f32x4*)(a.ws_o + (p * stride + hr) * D + dq * 4);
-      acc += w != 0.f ? w * v : f32x4{0.f, 0.f, 0.f, 0.f};
+    // this thread's parts pg, pg + PG, ... (at most kPartsPerThread): every
+    // load is issued before the first is used, so the row costs one memory
+    // latency; the sum runs over the parts in the same order as a plain loop
+    float w[kPartsPerThread];
+    f32x4 v[kPartsPerThread];
+#pragma unroll
+    for (int i = 0; i < kPartsPerThread; ++i) {
+      // unconditional loads (a part past the last, or one that saw no key and
+      // left its slot unwritten, reads a slot in range and gets weight 0; the
+      // select below drops whatever it holds)
+      const int p = pg + i * PG;
+      const int pc = min(p, a.splits - 1);
+      w[i] = p < a.splits ? w_s[r][p] : 0.f;
+      v[i] = *(const f32x4*)(a.ws_o + (pc * stride + hr) * D + dq * 4);
     }
+#pragma unroll
+    for (int i = 0; i < kPartsPerThread; ++i)
+      if (pg + i * PG < a.splits) acc += w[i] != 0.f ? w[i] * v[i] : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   acc_s[tid] = acc;
   __syncthreads();
@@ -169,6 +183,7 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
   const int nq = a.D / 4;
   int pg = 1;
   while (pg < a.splits && pg * 2 * nq <= kMergeThreads) pg *= 2;
+  if (pg * kPartsPerThread < a.splits) return hipErrorInvalidValue;
   const int rpb = kMergeThreads / (nq * pg);
   const int blocks = (int)((rows + rpb - 1) / rpb);
   if (a.D == 128)
