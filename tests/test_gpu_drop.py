@@ -253,3 +253,48 @@ def test_drop_with_workspace_replays_as_a_graph():
         torch.cuda.synchronize()
         k, i0, o, n = eager[0]
         assert int(cnt.item()) == n and torch.equal(keep, k) and torch.equal(idx[:n], i0) and torch.equal(out[:n], o)
+
+
+def test_single_pass_back_to_back_and_concurrent_calls():
+    """Calls queued back to back on one stream with one workspace, and calls on
+    two streams at once with their own workspaces: every call's words carry
+    its own tag, so each result is that of the two passes on its inputs."""
+    shapes = [(12, 4, 64, 512), (5, 4, 40, 512), (12, 4, 64, 512)]
+    frames = [make_drop_frames(*s, seed=41 + i) for i, s in enumerate(shapes)]
+    want = [run_gpu(f, 0.9, schedule="two_pass") for f in frames]
+
+    def prepare(bits):
+        B, C, n_f, dm = bits.shape
+        return dict(fr=dev(bits), keep=torch.full((B, n_f), 7, dtype=torch.uint8, device="cuda"),
+                    idx=torch.full((B * C * n_f,), -5, dtype=torch.int32, device="cuda"),
+                    cnt=torch.full((1,), -1, dtype=torch.int32, device="cuda"),
+                    out=torch.zeros((B * C * n_f, dm), dtype=torch.bfloat16, device="cuda"))
+
+    def launch(o, ws, stream):
+        with torch.cuda.stream(stream):
+            vico.vico_temporal_drop(o["fr"], 0.9, o["keep"], o["idx"], o["cnt"], out_tokens=o["out"], workspace=ws,
+                                    stream=stream)
+
+    def same(o, w):
+        n = int(o["cnt"].item())
+        assert n == w["n"]
+        assert np.array_equal(o["keep"].cpu().numpy(), w["keep"])
+        assert np.array_equal(o["idx"].cpu().numpy()[:n], w["idx"][:n])
+        assert np.array_equal(bits_of(o["out"][:n]), w["out"])
+
+    ws, ws2 = workspace_for(shapes[0], "single_pass"), workspace_for(shapes[0], "single_pass")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = [prepare(f) for f in frames]
+    torch.cuda.synchronize()
+    for o in outs:
+        launch(o, ws, s1)                                 # queued on s1, no wait between
+    torch.cuda.synchronize()
+    for o, w in zip(outs, want):
+        same(o, w)
+    o1, o2 = prepare(frames[0]), prepare(frames[2])
+    torch.cuda.synchronize()
+    launch(o1, ws, s1)
+    launch(o2, ws2, s2)
+    torch.cuda.synchronize()
+    same(o1, want[0])
+    same(o2, want[2])
