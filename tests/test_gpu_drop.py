@@ -147,6 +147,10 @@ def test_many_chunks_ranks_across_chunks(schedule):
     ((7, 3, 37, 4096), 0.9, False),      # 8 units of 512 features per lane, ragged tiles
     ((4, 8, 50, 2048), 0.5, False),      # C = 8 at its widest single-pass row
     ((9, 1, 13, 200), 0.8, False),       # C = 1 without a previous frame; 25 pieces of a row
+    ((9, 3, 1, 64), 0.5, False),         # one position per frame: every group leads its chunk
+    ((7, 4, 3, 128), 0.5, False),        # one ragged tile per chunk
+    ((256, 2, 4, 64), 0.9, False),       # the most chunks the single pass takes: a look-back of 4 windows
+    ((6, 4, 37, 8), 0.5, False),         # 8 features: one lane of a wave holds the row
 ])
 def test_schedules_agree_bit_for_bit(shape, tau, with_prev):
     """Both schedules run the same arithmetic: every output is the same bits,
