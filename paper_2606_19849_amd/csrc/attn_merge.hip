@@ -49,15 +49,18 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs
   const int dq = (int)(idx % NQ);
   const int64_t hr = idx / NQ;
   // every part's lse and O of this thread are loaded together (up to
-  // kFewParts, unrolled), so one memory latency covers the whole row
+  // kFewParts, unrolled), so one memory latency covers the whole row.  The O
+  // loads do not wait for the lse values: a part past the last reads the last
+  // part's slot, and an empty part (lse = -inf, its O slot possibly never
+  // written) is dropped by the select in the sum, whatever its slot holds.
   float ls[kFewParts];
   f32x4 os[kFewParts];
 #pragma unroll
-  for (int s = 0; s < kFewParts; ++s) ls[s] = s < a.splits ? a.ws_lse[s * n_rows + hr] : -INFINITY;
-#pragma unroll
-  for (int s = 0; s < kFewParts; ++s)
-    // an empty part (lse = -inf) may never have written its O slot: not read
-    os[s] = ls[s] != -INFINITY ? *(const f32x4*)(a.ws_o + (s * n_rows + hr) * D + dq * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < kFewParts; ++s) {
+    const int sc = min(s, a.splits - 1);
+    ls[s] = s < a.splits ? a.ws_lse[s * n_rows + hr] : -INFINITY;
+    os[s] = *(const f32x4*)(a.ws_o + (sc * n_rows + hr) * D + dq * 4);
+  }
   float mx = -INFINITY;
 #pragma unroll
   for (int s = 0; s < kFewParts; ++s) mx = fmaxf(mx, ls[s]);
@@ -68,7 +71,7 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs
   for (int s = 0; s < kFewParts; ++s) {
     const float w = ls[s] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ls[s] - m_use);
     wsum += w;
-    acc += w * os[s];
+    acc += ls[s] == -INFINITY ? f32x4{0.f, 0.f, 0.f, 0.f} : w * os[s];
   }
   acc *= wsum > 0.f ? 1.f / wsum : 0.f;
   const int row = (int)(hr % a.C);
