@@ -54,29 +54,38 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// one wave per chunk (grid-stride over chunks)
+// One wave per chunk (grid-stride over chunks).  |q|^2, <q, c_i> and |c_i|^2
+// are summed in one walk over the features, kScoreBatch float4 of q and of
+// the row per lane loaded before any is used, so a 3584-feature row costs two
+// memory latencies.  Each lane adds its columns in increasing order and the
+// wave reduction is fixed, so every wave gets the same |q|^2 bits.
+constexpr int kScoreBatch = 8;
 __global__ __launch_bounds__(256) void chunk_scores_kernel(const float* __restrict__ qf, const float* __restrict__ cf,
                                                            int N, int dm, float* __restrict__ scores) {
   const int lane = threadIdx.x & 63;
   const int gw = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int nw = (gridDim.x * blockDim.x) >> 6;
   const int n4 = dm / 4;
-  float qq = 0.f;
-  for (int c = lane; c < n4; c += 64) {
-    const f32x4 q = *(const f32x4*)(qf + 4 * c);
-    qq += q[0] * q[0] + q[1] * q[1] + q[2] * q[2] + q[3] * q[3];
-  }
-  qq = wave_sum(qq);
   for (int i = gw; i < N; i += nw) {
     const float* row = cf + (int64_t)i * dm;
-    float dot = 0.f, cc = 0.f;
-#pragma unroll 4
-    for (int c = lane; c < n4; c += 64) {
-      const f32x4 q = *(const f32x4*)(qf + 4 * c);
-      const f32x4 v = *(const f32x4*)(row + 4 * c);
-      dot += q[0] * v[0] + q[1] * v[1] + q[2] * v[2] + q[3] * v[3];
-      cc += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+    float dot = 0.f, cc = 0.f, qq = 0.f;
+    for (int c0 = lane; c0 < n4; c0 += 64 * kScoreBatch) {
+      f32x4 q[kScoreBatch], v[kScoreBatch];
+#pragma unroll
+      for (int u = 0; u < kScoreBatch; ++u) {
+        const int c = min(c0 + 64 * u, n4 - 1);      // in range; the sums below skip c >= n4
+        q[u] = *(const f32x4*)(qf + 4 * c);
+        v[u] = *(const f32x4*)(row + 4 * c);
+      }
+#pragma unroll
+      for (int u = 0; u < kScoreBatch; ++u)
+        if (c0 + 64 * u < n4) {
+          qq += q[u][0] * q[u][0] + q[u][1] * q[u][1] + q[u][2] * q[u][2] + q[u][3] * q[u][3];
+          dot += q[u][0] * v[u][0] + q[u][1] * v[u][1] + q[u][2] * v[u][2] + q[u][3] * v[u][3];
+          cc += v[u][0] * v[u][0] + v[u][1] * v[u][1] + v[u][2] * v[u][2] + v[u][3] * v[u][3];
+        }
     }
+    qq = wave_sum(qq);
     dot = wave_sum(dot);
     cc = wave_sum(cc);
     if (lane == 0) {
