@@ -137,7 +137,7 @@ def _check_topk_exact(scores32, k, tau=-math.inf, table=True):
         assert np.all(r["seg_len"][n:] == 0) and np.all(r["seg_start"][n:] == 0)
 
 
-@pytest.mark.parametrize("N", [1, 5, 1000, 1024, 5000, 100000])
+@pytest.mark.parametrize("N", [1, 5, 256, 257, 1000, 1024, 5000, 100000])   # 256 threads up to 256 scores
 @pytest.mark.parametrize("k", [1, 7, 32, 2048])
 def test_topk_matches_oracle_rule_on_fp32_scores(N, k):
     rng = np.random.default_rng(N * 7 + k)
