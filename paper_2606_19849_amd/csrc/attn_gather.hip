@@ -105,15 +105,27 @@ __global__ __launch_bounds__(kGatherThreads, 1) void attn_gather_kernel(GatherAr
 
   // ---- segment table: clamp every segment to the store, prefix-sum lengths
   {
+    // every entry of this thread is loaded before any is used (one memory
+    // latency); an index past the table reads its last entry and counts as
+    // empty.  With no segments the table pointers may be null: no loads.
     int len[SEG_PER_THREAD], run = 0;
+    int64_t st[SEG_PER_THREAD];
+    int32_t sl[SEG_PER_THREAD];
+    if (a.n_segs > 0) {
+#pragma unroll
+      for (int e = 0; e < SEG_PER_THREAD; ++e) {
+        const int ic = min(tid * SEG_PER_THREAD + e, a.n_segs - 1);
+        st[e] = a.seg_start[ic];
+        sl[e] = a.seg_len[ic];
+      }
+    }
 #pragma unroll
     for (int e = 0; e < SEG_PER_THREAD; ++e) {
       const int i = tid * SEG_PER_THREAD + e;
       int n = 0, slot = 0;
       if (i < a.n_segs) {
-        const int64_t st = a.seg_start[i];
-        const int64_t lo = st > 0 ? st : 0;
-        const int64_t en = st + (int64_t)a.seg_len[i];
+        const int64_t lo = st[e] > 0 ? st[e] : 0;
+        const int64_t en = st[e] + (int64_t)sl[e];
         const int64_t hi = en < (int64_t)a.cap ? en : (int64_t)a.cap;
         if (hi > lo) { n = (int)(hi - lo); slot = (int)lo; }
       }
