@@ -13,6 +13,15 @@ example, so these are the stored values.
       row sees: the bounded visible set of Sec. 3 ("LLM Prefilling and
       Decoding"), token-granular with the causal chunk, read through a ring
       that has wrapped.  LSE = ln(number of visible keys).
+  gather_uniform.json
+      Short-query attention over sink ++ store segments ++ causal tail with
+      Q = 0 (the query-time attention of Sec. 3 over the retrieved chunks):
+      each output row is the mean of the V rows of the sink, of the store
+      slots the segments list (in table order, an empty segment included)
+      and of tail tokens 0 .. T-Lq+i.  A 3-row query and a decode step.
+      The table handed to the library ("table_start"/"table_len") also has
+      segments reaching outside the store, which the library clips to it;
+      the oracle gets the clipped table ("seg_start"/"seg_len").
   acn_windows.json
       The chunk-granular window of Eq. (4): the history tokens of chunks
       t-acn .. t-1 for a ragged table of chunk starts.
@@ -70,6 +79,41 @@ def attention_uniform_cases():
             "cases": cases}
 
 
+def gather_uniform_cases():
+    cases = []
+    for name, (Hq, Hkv, d, S, cap, segs, T, Lq, bases) in {
+        "query": (4, 2, 64, 2, 48, [(30, 5), (2, 7), (15, 0), (40, 12), (-3, 5), (50, 4), (10, -2)], 6, 3,
+                  (100, 120, 30)),
+        "decode": (2, 1, 128, 1, 20, [(0, 20)], 4, 1, (10, 20, 60)),
+    }.items():
+        b_sink, b_store, b_tail = bases
+
+        def rows(base, n):
+            v = np.zeros((n, Hkv, d))
+            for i in range(n):
+                v[i] = base + i + np.arange(d)[None, :]
+            return v
+
+        z = lambda n: np.zeros((n, Hkv, d))
+        # the library's contract for a table entry: slots [max(0, a), min(a + n, cap)), empty if none
+        clipped = [(max(0, a), min(a + n, cap) - max(0, a)) if min(a + n, cap) > max(0, a) else (0, 0)
+                   for a, n in segs]
+        starts = [a for a, _ in clipped]
+        lens = [n for _, n in clipped]
+        out, lse = oracle.gather_attention(np.zeros((Lq, Hq, d)), z(T), rows(b_tail, T), z(S), rows(b_sink, S),
+                                           z(cap), rows(b_store, cap), starts, lens)
+        cases.append({
+            "name": name, "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": d, "sink_len": S,
+            "store_slots": cap, "table_start": [a for a, _ in segs], "table_len": [n for _, n in segs],
+            "seg_start": starts, "seg_len": lens, "tail_len": T, "q_len": Lq,
+            "bases": {"sink": b_sink, "store": b_store, "tail": b_tail},
+            "value_rule": "v[key][kv][c] = base + index + c (index: sink s, store slot, tail token t)",
+            "out_column0": out[:, :, 0].tolist(),
+            "lse": lse.tolist(),
+        })
+    return {"citation": "Sec. 3, query-time decoding (attention over the retrieved chunks)", "cases": cases}
+
+
 def acn_cases():
     starts = [0, 300, 300, 1324, 1580, 2604, 2860, 3116]     # ragged chunk lengths, one empty chunk
     table = []
@@ -105,7 +149,8 @@ def drop_cases():
 
 
 def main():
-    for fn, data in (("attention_uniform.json", attention_uniform_cases()), ("acn_windows.json", acn_cases()),
+    for fn, data in (("attention_uniform.json", attention_uniform_cases()), ("gather_uniform.json", gather_uniform_cases()),
+                     ("acn_windows.json", acn_cases()),
                      ("drop_exact_cosines.json", drop_cases())):
         with open(os.path.join(HERE, fn), "w") as f:
             json.dump(data, f, indent=1)

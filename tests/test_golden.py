@@ -51,6 +51,28 @@ def test_attention_uniform_fixture(case):
     assert np.allclose(lse, case["lse"], rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("case", load("gather_uniform.json")["cases"], ids=lambda c: c["name"])
+def test_gather_uniform_fixture(case):
+    S, T, Lq, Hq = case["sink_len"], case["tail_len"], case["q_len"], case["num_q_heads"]
+    b = case["bases"]
+    cap = case["store_slots"]
+    store_keys = [b["store"] + slot for a, n in zip(case["table_start"], case["table_len"])
+                  for slot in range(a, a + n) if 0 <= slot < cap]         # the part of each entry inside the store
+    for i in range(Lq):
+        keys = [b["sink"] + s for s in range(S)] + store_keys + [b["tail"] + t for t in range(T - Lq + i + 1)]
+        want = Fraction(sum(keys), len(keys))
+        for h in range(Hq):
+            assert case["out_column0"][i][h] == pytest.approx(float(want), rel=0, abs=1e-12)
+            assert case["lse"][h][i] == pytest.approx(math.log(len(keys)), rel=0, abs=1e-12)
+    Hkv, d = case["num_kv_heads"], case["head_dim"]
+    rows = lambda base, n: np.stack([np.full((Hkv, d), base + i) + np.arange(d) for i in range(n)])
+    z = lambda n: np.zeros((n, Hkv, d))
+    out, lse = oracle.gather_attention(np.zeros((Lq, Hq, d)), z(T), rows(b["tail"], T), z(S), rows(b["sink"], S),
+                                       z(cap), rows(b["store"], cap), case["seg_start"], case["seg_len"])
+    assert np.allclose(out[:, :, 0], case["out_column0"], rtol=0, atol=1e-12)
+    assert np.allclose(lse, case["lse"], rtol=0, atol=1e-12)
+
+
 def test_acn_window_fixture():
     g = load("acn_windows.json")
     starts = g["chunk_starts"]

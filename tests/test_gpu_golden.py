@@ -60,6 +60,34 @@ def test_attention_uniform_golden(case, out_dtype):
     assert np.allclose(lse.cpu().numpy(), case["lse"], rtol=2.0 ** -20, atol=0)
 
 
+@pytest.mark.parametrize("case", load("gather_uniform.json")["cases"], ids=lambda c: c["name"])
+@pytest.mark.parametrize("parts", [0, 1, 3])
+def test_gather_uniform_golden(case, parts):
+    Hq, Hkv, d, S, cap, T, Lq = (case[k] for k in ("num_q_heads", "num_kv_heads", "head_dim", "sink_len",
+                                                   "store_slots", "tail_len", "q_len"))
+    b = case["bases"]
+    zeros = lambda n, h: torch.zeros((n, h, d), dtype=torch.bfloat16, device="cuda")
+    q = zeros(Lq, Hq)
+    tk, tv = zeros(T, Hkv), bf16_rows(b["tail"], T, Hkv, d)
+    sk, sv = zeros(S, Hkv), bf16_rows(b["sink"], S, Hkv, d)
+    gk, gv = zeros(cap, Hkv), bf16_rows(b["store"], cap, Hkv, d)
+    ss = torch.tensor(case["table_start"], dtype=torch.int64, device="cuda")    # clipped by the library
+    sl = torch.tensor(case["table_len"], dtype=torch.int32, device="cuda")
+    hint = int(sum(case["seg_len"]))
+    np_, wb = vico.vico_gather_plan(Lq, T, S, cap, len(case["table_start"]), hint, Hq, Hkv, d, num_splits=parts)
+    ws = torch.empty(max(wb, 256), dtype=torch.uint8, device="cuda")
+    out = torch.empty((Lq, Hq, d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((Hq, Lq), dtype=torch.float32, device="cuda")
+    vico.vico_gather_attn(q, tk, tv, sk, sv, gk, gv, ss, sl, out, lse=lse, workspace=ws, keys_hint=hint,
+                          num_splits=parts)
+    torch.cuda.synchronize()
+    want = np.asarray(case["out_column0"])[:, :, None] + np.arange(d)[None, None, :]
+    got = out.cpu().numpy().astype(np.float64)
+    tol = 2.0 ** -23 if np_ == 1 else 2.0 ** -20      # the merge of parts adds a few fp32 roundings
+    assert np.max(np.abs(got - want) / want) <= tol
+    assert np.allclose(lse.cpu().numpy(), case["lse"], rtol=2.0 ** -20, atol=0)
+
+
 @pytest.mark.parametrize("schedule", ["two_pass", "single_pass"])
 def test_drop_exact_cosines_golden(schedule):
     g = load("drop_exact_cosines.json")
