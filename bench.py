@@ -104,6 +104,22 @@ class Busy:
         self.launch(max(1, ms / self.ms_per_iter), stream)
 
 
+def back_to_back(torch, busy, stream, call, first, steps, hold_ms):
+    """Seconds per call of call(first) .. call(first + steps - 1) launched back
+    to back, with an event only before the first and after the last: an
+    event recorded between two launches costs the GPU 2-3 us, a tenth of a
+    short call.  A hold of `hold_ms` of matrix work first lets the host
+    enqueue every call before the GPU reaches them."""
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    busy.hold(stream, ms=hold_ms)
+    a.record(stream)
+    for j in range(steps):
+        call(first + j)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e-3 / steps
+
+
 def warm_up(torch, call, min_steps, seconds):
     """Run `call(i)` for at least `min_steps` calls and `seconds` of wall time,
     back to back, so the timed loop starts with the GPU at its loaded clock
@@ -400,7 +416,12 @@ def run_ramp_study(args, torch, vico):
 
 
 def run_stream_workload(args, torch, vico):
-    """64 ragged chunks at the 3B shape: per-chunk latency vs chunk index."""
+    """64 ragged chunks at the 3B shape: aggregate visual tokens/s, and
+    per-chunk latency vs chunk index.  Each repetition replays the stream
+    twice: once with events only before the first and after the last chunk
+    (the aggregate rate: an event recorded between two launches costs the
+    GPU 2-3 us, 5 % of a chunk), and once with one event per chunk boundary
+    (the per-chunk latencies and their drift)."""
     from synth import ragged_chunk_lengths, stream_chunk, stream_sink
     dev = lambda bits: _dev(torch, bits)
     Hq, Hkv, D, S, W, R = 16, 2, 128, 64, 8192, 8192
@@ -419,26 +440,36 @@ def run_stream_workload(args, torch, vico):
         outs = [torch.empty((int(c), Hq, D), dtype=torch.bfloat16, device="cuda") for c in counts]
         stream = torch.cuda.current_stream()
         lat = np.zeros((args.steps, len(counts)))
+        whole = np.zeros(args.steps)
         busy = Busy(torch)
         t_warm = time.perf_counter()
         rep, n_warm = 0, None
+
+        def chunk(t):
+            q, k, v = chunks[t]
+            # attend, then append the chunk to the ring, in one call
+            vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, int(starts[t]), window, outs[t],
+                                         workspace=ws, stream=stream, flags=vico.VICO_ATTN_APPEND)
+
         while n_warm is None or rep < n_warm + args.steps:
             if n_warm is None and rep >= args.warmup and time.perf_counter() - t_warm >= args.warmup_seconds:
                 n_warm = rep
-            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-                   torch.cuda.Event(enable_timing=True)) for _ in counts]
+            ends = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
             busy.hold(stream, ms=6.0)
-            for t, c in enumerate(counts):
-                q, k, v = chunks[t]
-                ev[t][0].record(stream)
-                # attend, then append the chunk to the ring, in one call
-                vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, int(starts[t]), window, outs[t],
-                                             workspace=ws, stream=stream, flags=vico.VICO_ATTN_APPEND)
-                ev[t][1].record(stream)
-                ev[t][2].record(stream)
+            ends[0].record(stream)
+            for t in range(len(counts)):
+                chunk(t)
+            ends[1].record(stream)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(counts) + 1)]
+            busy.hold(stream, ms=6.0)
+            ev[0].record(stream)
+            for t in range(len(counts)):
+                chunk(t)
+                ev[t + 1].record(stream)
             torch.cuda.synchronize()
             if n_warm is not None:
-                lat[rep - n_warm] = [e[0].elapsed_time(e[2]) for e in ev]
+                whole[rep - n_warm] = ends[0].elapsed_time(ends[1])
+                lat[rep - n_warm] = [a.elapsed_time(b) for a, b in zip(ev, ev[1:])]
             rep += 1
         med = np.median(lat, axis=0)
         flops = np.array([attn_flops(int(c), S, min(int(starts[t]), W) if window >= 0 else int(starts[t]), Hq, D)
@@ -449,8 +480,10 @@ def run_stream_workload(args, torch, vico):
         X = np.stack([np.ones(sel.sum()), flops[sel], t_idx[sel]], 1)
         coef = np.linalg.lstsq(X, med[sel], rcond=None)[0]
         res_all[mode] = {
+            "stream_ms": round(float(np.median(whole)), 4),
+            "tokens_per_s": round(float(counts.sum() / (np.median(whole) * 1e-3)), 1),
             "per_chunk_ms": [round(float(x), 4) for x in med],
-            "tokens_per_s": round(float(counts.sum() / (med.sum() * 1e-3)), 1),
+            "tokens_per_s_chunk_events": round(float(counts.sum() / (med.sum() * 1e-3)), 1),
             "tflops_per_chunk": [round(float(f / (m * 1e-3) / 1e12), 1) for f, m in zip(flops, med)],
             "drift_ms_over_64_chunks": round(float(coef[2] * 63), 4),
             "mean_ms": round(float(med.mean()), 4),
@@ -460,7 +493,7 @@ def run_stream_workload(args, torch, vico):
         "metric": "chunk-prefill attention TFLOP/s (% bf16 MFMA peak) + visual tokens/s per layer",
         "value": b["tokens_per_s"], "unit": "visual tokens/s per layer",
         "n_gpus": 1, "steps": args.steps, "warmup": n_warm,
-        "ms_per_step": round(sum(b["per_chunk_ms"]), 4),
+        "ms_per_step": b["stream_ms"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": DESCR["stream"], "chunks": len(counts), "tokens": int(counts.sum())},
@@ -539,6 +572,7 @@ def run_query_workload(args, torch, vico):
 
     n_warm = warm_up(torch, step, args.warmup, args.warmup_seconds)
     busy = Busy(torch)
+    # per-call events (retrieval and attention of each step apart)
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -547,9 +581,14 @@ def run_query_workload(args, torch, vico):
         step(n_warm + j, ev[j])
     torch.cuda.synchronize()
     host_paced = args.steps / (time.perf_counter() - t0)
-    elapsed = ev[0][0].elapsed_time(ev[-1][2]) * 1e-3          # GPU span of the steps, fed ahead
     ret_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
     att_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    # the same K calls with no events between them (the value and the roofline)
+    hold_ms = max(4.0, 1.25e3 * args.steps / host_paced)
+    lean = lambda call: back_to_back(torch, busy, stream, call, n_warm, args.steps, hold_ms)
+    step_s = lean(step)
+    attn_s = lean(lambda j: attend(qs[j % n_q]))
+    ret_s = None if decode else lean(lambda j: retrieve(qs[j % n_q]))
     Hq, Hkv, D, S, T = sh.num_q_heads, sh.num_kv_heads, sh.head_dim, sh.sink_len, sh.tail_len
     G = np.array([gathered[(n_warm + j) % n_q] for j in range(args.steps)], dtype=np.float64)
     keys = S + G + T
@@ -557,24 +596,26 @@ def run_query_workload(args, torch, vico):
     bytes_ = kv_bytes + Lq * Hq * D * 2 * 2 + Hq * Lq * 4            # + Q, O (bf16), LSE
     rows = T - Lq + np.arange(Lq) + 1                                   # visible tail keys per query row
     flops = np.array([4.0 * Hq * D * float(np.sum(S + g + rows)) for g in G])
-    gbs = float(np.mean(bytes_ / (att_ms * 1e-3)) / 1e9)
-    tfl = float(np.mean(flops / (att_ms * 1e-3)) / 1e12)
+    gbs = float(bytes_.mean() / attn_s / 1e9)
+    tfl = float(flops.mean() / attn_s / 1e12)
     t_hbm = bytes_.mean() / (PEAK_HBM_GBS * 1e9)
     t_mfma = flops.mean() / (PEAK_BF16_TFLOPS * 1e12)
     res = {
         "metric": ("decode-step attention per layer" if decode else
                    "query-side retrieval + gathered attention per layer (TTFT building block)"),
-        "value": round(args.steps / elapsed, 1), "unit": "steps/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "value": round(1.0 / step_s, 1), "unit": "steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(step_s * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": DESCR[args.workload], "q_rows": Lq, "tail": T, "top_k": sh.top_k,
                    "stored_chunks": sh.num_chunks, "store_tokens": qi0.store_len, "parts": parts,
                    "gathered_keys_mean": float(G.mean())},
         "host_paced_steps_per_s": round(host_paced, 1),
-        "retrieval_us_mean": None if decode else round(float(ret_ms.mean()) * 1e3, 2),
-        "attn_us_mean": round(float(att_ms.mean()) * 1e3, 2),
-        "attn_us_median": round(float(np.median(att_ms)) * 1e3, 2),
+        "retrieval_us_mean": None if decode else round(ret_s * 1e6, 2),
+        "attn_us_mean": round(attn_s * 1e6, 2),
         "attn_tflops": round(tfl, 2),
+        "per_call_events": {"retrieval_us_mean": None if decode else round(float(ret_ms.mean()) * 1e3, 2),
+                            "attn_us_mean": round(float(att_ms.mean()) * 1e3, 2),
+                            "attn_us_median": round(float(np.median(att_ms)) * 1e3, 2)},
         "roofline": {"bound": "hbm" if t_hbm >= t_mfma else "mfma",
                      "achieved": round(gbs, 1) if t_hbm >= t_mfma else round(tfl, 2),
                      "peak": PEAK_HBM_GBS if t_hbm >= t_mfma else PEAK_BF16_TFLOPS,
@@ -631,21 +672,26 @@ def run_drop_workload(args, torch, vico):
     if int(cnt.item()) != kept[(n_warm + args.steps - 1) % n_batches]:
         raise RuntimeError("temporal drop: the last timed call retained a different count")
     host_paced = B * C * n_f * args.steps / (time.perf_counter() - t0)
-    elapsed = ev[0][0].elapsed_time(ev[-1][1]) * 1e-3          # GPU span of the calls, fed ahead
     ms = np.array([a.elapsed_time(b) for a, b in ev])
+    # the same K calls with no events between them (the value and the roofline)
+    call_s = back_to_back(torch, busy, stream, lambda j: call(batches[j % n_batches]), n_warm, args.steps,
+                          max(4.0, 1.25e3 * args.steps * B * C * n_f / host_paced))
+    if int(cnt.item()) != kept[(n_warm + args.steps - 1) % n_batches]:
+        raise RuntimeError("temporal drop: the last timed call retained a different count")
     n_keep = np.array([kept[(n_warm + j) % n_batches] for j in range(args.steps)], dtype=np.float64)
     in_bytes = B * C * n_f * dm * 2
     alg = in_bytes + n_keep * (dm * 2 + 4) + B * n_f
-    gbs = float(np.mean(alg / (ms * 1e-3)) / 1e9)
+    gbs = float(alg.mean() / call_s / 1e9)
     kernel = "drop_fused_kernel<4, 7>" if single else "drop_sim_kernel<4>"
     return {
         "metric": "temporal token dropping throughput (input tokens/s)",
-        "value": round(B * C * n_f * args.steps / elapsed, 1), "unit": "tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "value": round(B * C * n_f / call_s, 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(call_s * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": DESCR["drop"], "retention": round(float(n_keep.mean()) / (B * C * n_f), 4),
                    "schedule": args.drop_schedule},
-        "call_us_mean": round(float(ms.mean()) * 1e3, 2),
+        "call_us_mean": round(call_s * 1e6, 2),
+        "per_call_events": {"call_us_mean": round(float(ms.mean()) * 1e3, 2)},
         "host_paced_tokens_per_s": round(host_paced, 1),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_HBM_GBS, 4),
@@ -678,17 +724,22 @@ def run_append_workload(args, torch, vico):
         vico.vico_kv_append(k, v, rk, rv, 777 + i * 1000, stream=stream)
         ev[i][1].record(stream)
     torch.cuda.synchronize()
-    host_paced = 2 * 2 * C * Hkv * D * 2 * args.steps / (time.perf_counter() - t0) / 1e9
-    elapsed = ev[0][0].elapsed_time(ev[-1][1]) * 1e-3          # GPU span of the calls, fed ahead
+    wall = time.perf_counter() - t0
+    host_paced = 2 * 2 * C * Hkv * D * 2 * args.steps / wall / 1e9
     ms = np.array([a.elapsed_time(b) for a, b in ev])
     nbytes = 2 * 2 * C * Hkv * D * 2
-    gbs = nbytes / (ms.mean() * 1e-3) / 1e9
+    # the same K calls with no events between them (the value and the roofline)
+    call_s = back_to_back(torch, busy, stream, lambda i: vico.vico_kv_append(k, v, rk, rv, 777 + i * 1000,
+                                                                             stream=stream),
+                          0, args.steps, max(4.0, 1.25e3 * wall))
+    gbs = nbytes / call_s / 1e9
     return {
-        "metric": "ring append HBM GB/s", "value": round(nbytes * args.steps / elapsed / 1e9, 1), "unit": "GB/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "metric": "ring append HBM GB/s", "value": round(gbs, 1), "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": n_warm, "ms_per_step": round(call_s * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "ring append at capacity: 16384 tokens x 4 kv heads x d128, K and V, ring wraps",
                    "bytes_per_launch": nbytes},
+        "per_call_events": {"GBps": round(nbytes / (ms.mean() * 1e-3) / 1e9, 1)},
         "host_paced_GBps": round(host_paced, 1),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_HBM_GBS, 4),

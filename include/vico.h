@@ -107,7 +107,7 @@ int vico_kv_append(const void* k_chunk, const void* v_chunk, int32_t chunk_len,
  *                  exp(scale * q.k) over the visible keys of each row
  *   num_splits     0: the library picks the schedule; n > 0 splits every row
  *                  tile's key range into n parts (clamped to the number of key
- *                  tiles); VICO_SPLIT_BALANCED gives every work-group an equal
+ *                  tiles and to 16); VICO_SPLIT_BALANCED gives every work-group an equal
  *                  share of all key tiles of all row tiles.  Split or shared
  *                  row tiles are combined by a log-sum-exp merge.  Results
  *                  agree up to rounding for every choice.

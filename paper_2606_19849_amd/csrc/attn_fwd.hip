@@ -8,9 +8,14 @@
 //
 // Mapping onto the hardware
 //   * Work-group = 8 waves (two per SIMD, one work-group per CU) = 256 query
-//     rows of one query head (one key range when split).  Each wave owns 32
-//     rows for the whole key loop; every K/V tile brought into LDS serves all
-//     256 rows.
+//     rows (one key range when split).  Each wave owns 32 rows for the whole
+//     key loop; every K/V tile brought into LDS serves all 256 rows.  The
+//     rows are 256 tokens of one query head, or -- when the chunk length is
+//     not a multiple of 256, so that the last row tile of every query head
+//     would be part-empty -- packed (token, head) pairs of all query heads of
+//     one KV head, token-major (row r: token r / g, head kv*g + r % g), which
+//     leaves one part-filled row tile per KV head instead.  Both forms read
+//     the same K/V; the packed one is its own kernel, attn_fwd_packed_kernel.
 //   * The tile body (S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_32x32x16_bf16,
 //     the exponentiate-first online softmax, two 32-key halves) is WaveTile
 //     of attn_common.h, shared with the gathered-query kernel.
@@ -29,7 +34,8 @@
 //     literally: a chunk sees all of itself) every row's last key is the
 //     chunk's last key, so only the tile holding the chunk end is masked.
 //   * Work-groups are renumbered so that consecutive logical ids (the query
-//     heads of one KV head) land on the same XCD and share its L2.
+//     heads, or the packed row tiles, of one KV head) land on the same XCD
+//     and share its L2.
 //   * Optional split of the key range (for chunks too small to fill 256 CUs):
 //     each split writes fp32 O and log2-sum-exp; a merge kernel combines them.
 
@@ -40,8 +46,10 @@
 namespace vico {
 namespace {
 
-template <int D>
-__global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a, int n_rt, int g) {
+// The kernel body; PACKED selects the packed (token, head) rows.  Inlined
+// into one kernel per row form (attn_fwd_kernel, attn_fwd_packed_kernel).
+template <int D, bool PACKED>
+__device__ __forceinline__ void attn_fwd_body(const AttnArgs& a, int n_rt, int gq) {
   constexpr int BN = kKeyTile;         // keys per tile
   constexpr int BM = kBlockM;          // rows per work-group
   static_assert(kRowBlocks == 1, "one 32-row block per wave (the shared tile body)");
@@ -82,39 +90,48 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   const int l32 = lane & 31;
   const int hh = lane >> 5;
   const int C = a.C, S = a.S, SW = a.S + a.Wv;
+  const int P = PACKED ? a.pack : 1;   // query heads packed into the rows of a row tile
+  const int NR = C * P;                // packed rows of one head group
 
-  // last key visible to chunk row `row`: its own position (causal), or the
+  // last key visible to chunk token `tok`: its own position (causal), or the
   // chunk's last key when the chunk attends to itself bidirectionally
-  auto last_key_of_row = [&](int row) __attribute__((always_inline)) {
-    return SW + (a.bidir ? C - 1 : min(row, C - 1));
+  auto last_key_of_tok = [&](int tok) __attribute__((always_inline)) {
+    return SW + (a.bidir ? C - 1 : min(tok, C - 1));
   };
+  // packed row r of a head group is chunk token r / P of query head (group
+  // base) + r % P; rows past the group's end stand for its last row
+  auto tok_of = [&](int r) __attribute__((always_inline)) { return min(r, NR - 1) / P; };
   // key tiles seen by row tile rt: keys up to its last row's last key
   auto tiles_of = [&](int rt) __attribute__((always_inline)) {
-    return (last_key_of_row((rt + 1) * BM - 1) + BN) / BN;
+    return (last_key_of_tok(tok_of((rt + 1) * BM - 1)) + BN) / BN;
   };
 
-  // ---- one segment of work: key tiles [t_lo, t_hi) of row tile rt of query
-  // head h = kv*g + qh.  `partial` segments write fp32 O and log2-sum-exp to
-  // workspace slot `part` (of n_parts) for the merge kernel; others write the
-  // output.  All waves of the work-group run the same segments.
+  // ---- one segment of work: key tiles [t_lo, t_hi) of row tile rt of head
+  // group qh of KV head kv (query heads kv*g + qh*P .. + P-1).  `partial`
+  // segments write fp32 O and log2-sum-exp to workspace slot `part` (of
+  // n_parts) for the merge kernel; others write the output.  All waves of the
+  // work-group run the same segments.
   auto segment = [&](int kv, int rt, int qh, int t_lo, int t_hi, int part, int n_parts, bool partial)
       __attribute__((always_inline)) {
-  const int h = kv * g + qh;
+  const int h0 = (kv * gq + qh) * P;
   const int row0 = rt * BM;
   const int n_tiles = tiles_of(rt);
 
-  // this wave: rows wrow0 + l32
+  // this wave: packed rows wrow0 + l32; this lane: token tok of head h
   const int wrow0 = row0 + wave * 32;
-  const bool wave_active = wrow0 < C;
-  const int wave_first_lim = last_key_of_row(wrow0);              // last key of the wave's first row
-  const int wave_last_lim = last_key_of_row(wrow0 + 31);
-  const int key_lim = last_key_of_row(wrow0 + l32);
+  const bool wave_active = wrow0 < NR;
+  const int wave_first_lim = last_key_of_tok(tok_of(wrow0));      // last key of the wave's first row
+  const int wave_last_lim = last_key_of_tok(tok_of(wrow0 + 31));
+  const int my_row = min(wrow0 + l32, NR - 1);
+  const int tok = my_row / P;
+  const int h = h0 + my_row % P;
+  const int key_lim = last_key_of_tok(tok);
 
   // ---- the wave's Q rows and running state.  The Q loads are unconditional:
-  // rows past the chunk end repeat the last row (the clamped address) and are
-  // never stored, and a row's softmax only mixes the two lanes of that row.
+  // rows past the group's end repeat its last row (the clamped address) and
+  // are never stored, and a row's softmax only mixes the two lanes of that row.
   bf16x8 qf[WaveTile<D>::NKS];
-  WaveTile<D>::load_q(qf, a.q + ((int64_t)min(wrow0 + l32, C - 1) * a.Hq + h) * D + hh * 8);
+  WaveTile<D>::load_q(qf, a.q + ((int64_t)tok * a.Hq + h) * D + hh * 8);
 
   // ---- tile loader.  Direct load n of wave w fills LDS rows w*BN/4 + n*RPL ..
   // (RPL rows): lane i writes unit i % UPR of row w*BN/4 + n*RPL + i / UPR and
@@ -255,10 +272,10 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
 
   if (!wave_active) return;
   constexpr int NDB = WaveTile<D>::NDB;
-  const int row = wrow0 + l32;
+  const int row = tok;
   float inv, lse2;
   wt.finish(inv, lse2);
-  if (row >= C) return;
+  if (wrow0 + l32 >= NR) return;
   if (!partial) {
     if (a.out_f32) {
       float* op = (float*)a.out + ((int64_t)row * a.Hq + h) * D + hh * 4;
@@ -306,8 +323,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   if (!a.balanced) {
     // one row tile (one key range of it when split) per work-group
-    const int qh = L % g;
-    int rest = L / g;
+    const int qh = L % gq;
+    int rest = L / gq;
     const int rt = n_rt - 1 - rest % n_rt;   // longest row tiles first
     rest /= n_rt;
     const int sp = rest % a.splits;
@@ -318,7 +335,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
     segment(kv, rt, qh, t_lo, t_hi, sp, a.splits, a.splits > 1);
   } else {
     // Balanced: the (row tile, key tile) pairs of all row tiles, in the order
-    // kv, row tile (longest first), query head, are cut into gridDim.x equal
+    // kv, row tile (longest first), head group, are cut into gridDim.x equal
     // ranges.  A row tile cut between work-groups is finished by the merge
     // kernel; part = index of the work-group among those covering it.
     const int64_t G = gridDim.x, T = a.total_tiles;
@@ -332,7 +349,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
         for (int ri = 0; ri < n_rt; ++ri) {
           const int r = n_rt - 1 - ri;
           const int n = tiles_of(r);
-          const int64_t blk = (int64_t)g * n;
+          const int64_t blk = (int64_t)gq * n;
           if (pos >= base && pos < base + blk) {
             kv = k; rt = r; nt = n; qh = (int)((pos - base) / n);
           }
@@ -341,8 +358,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
       // start of the containing row tile in the global order
       int64_t task_start = 0;
       for (int k = 0; k < kv; ++k)
-        for (int ri = 0; ri < n_rt; ++ri) task_start += (int64_t)g * tiles_of(ri);
-      for (int ri = 0; ri < n_rt - 1 - rt; ++ri) task_start += (int64_t)g * tiles_of(n_rt - 1 - ri);
+        for (int ri = 0; ri < n_rt; ++ri) task_start += (int64_t)gq * tiles_of(ri);
+      for (int ri = 0; ri < n_rt - 1 - rt; ++ri) task_start += (int64_t)gq * tiles_of(n_rt - 1 - ri);
       task_start += (int64_t)qh * nt;
       const int lo = (int)(pos - task_start);
       const int hi = (int)(min(end, task_start + nt) - task_start);
@@ -355,15 +372,31 @@ __global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_kernel(AttnArgs a, int n_rt, int gq) {
+  attn_fwd_body<D, false>(a, n_rt, gq);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, kWgPerCU) void attn_fwd_packed_kernel(AttnArgs a, int n_rt, int gq) {
+  attn_fwd_body<D, true>(a, n_rt, gq);
+}
+
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t stream) {
   const int g = a.Hq / a.Hkv;
-  const int n_rt = (a.C + kBlockM - 1) / kBlockM;
-  if (a.D == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(grid), dim3(kThreads), 0, stream, a, n_rt, g);
-  else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(grid), dim3(kThreads), 0, stream, a, n_rt, g);
+  if (a.pack < 1 || g % a.pack != 0) return hipErrorInvalidValue;
+  const int gq = g / a.pack;
+  const int n_rt = (int)(((int64_t)a.C * a.pack + kBlockM - 1) / kBlockM);
+  const dim3 gr(grid), bl(kThreads);
+  if (a.pack == 1) {
+    if (a.D == 128) hipLaunchKernelGGL(attn_fwd_kernel<128>, gr, bl, 0, stream, a, n_rt, gq);
+    else hipLaunchKernelGGL(attn_fwd_kernel<64>, gr, bl, 0, stream, a, n_rt, gq);
+  } else {
+    if (a.D == 128) hipLaunchKernelGGL(attn_fwd_packed_kernel<128>, gr, bl, 0, stream, a, n_rt, gq);
+    else hipLaunchKernelGGL(attn_fwd_packed_kernel<64>, gr, bl, 0, stream, a, n_rt, gq);
+  }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (a.splits > 1) return launch_merge(a, stream);   // appends too, when asked

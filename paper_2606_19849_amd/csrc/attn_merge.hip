@@ -6,7 +6,7 @@
 // (a part that saw no key of the row carries lse_s = -inf and is skipped;
 // its O_s slot may never have been written).
 //
-// Few parts (up to 8, the chunk prefill splits) over many rows: one thread
+// Few parts (up to 16, the chunk prefill splits) over many rows: one thread
 // per 4 columns of a row loads all parts together.  Many parts (up to 64, short
 // queries): a thread walking them one by one is bound by load latency, so a
 // work-group of 256 threads takes RPB rows, and for each row PG groups of
@@ -22,7 +22,7 @@ namespace vico {
 namespace {
 
 constexpr int kMergeThreads = 256;
-constexpr int kFewParts = 8;     // up to here one thread per (row, 4 columns) loads all parts
+constexpr int kFewParts = 16;    // up to here one thread per (row, 4 columns) loads all parts
 constexpr int kPartsPerThread = 8;   // many parts: parts one thread loads (64 parts over 8 part groups)
 
 // With an append requested, the blocks past `merge_blocks` copy the chunk's
@@ -39,7 +39,7 @@ __device__ __forceinline__ bool append_block(const AttnArgs& a, int merge_blocks
 // Few parts, many rows (chunk prefill splits): one thread per (head, row,
 // 4-column group) reads every part's value at once; neighbouring threads
 // read neighbouring columns, so every load is a full coalesced row.
-template <int D>
+template <int D, int NP>
 __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs a, int merge_blocks) {
   if (append_block(a, merge_blocks)) return;
   constexpr int NQ = D / 4;
@@ -48,27 +48,27 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs
   if (idx >= n_rows * NQ) return;
   const int dq = (int)(idx % NQ);
   const int64_t hr = idx / NQ;
-  // every part's lse and O of this thread are loaded together (up to
-  // kFewParts, unrolled), so one memory latency covers the whole row.  The O
+  // every part's lse and O of this thread are loaded together (NP >= the
+  // parts, unrolled), so one memory latency covers the whole row.  The O
   // loads do not wait for the lse values: a part past the last reads the last
   // part's slot, and an empty part (lse = -inf, its O slot possibly never
   // written) is dropped by the select in the sum, whatever its slot holds.
-  float ls[kFewParts];
-  f32x4 os[kFewParts];
+  float ls[NP];
+  f32x4 os[NP];
 #pragma unroll
-  for (int s = 0; s < kFewParts; ++s) {
+  for (int s = 0; s < NP; ++s) {
     const int sc = min(s, a.splits - 1);
     ls[s] = s < a.splits ? a.ws_lse[s * n_rows + hr] : -INFINITY;
     os[s] = *(const f32x4*)(a.ws_o + (sc * n_rows + hr) * D + dq * 4);
   }
   float mx = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < kFewParts; ++s) mx = fmaxf(mx, ls[s]);
+  for (int s = 0; s < NP; ++s) mx = fmaxf(mx, ls[s]);
   const float m_use = (mx == -INFINITY) ? 0.f : mx;
   f32x4 acc{0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
 #pragma unroll
-  for (int s = 0; s < kFewParts; ++s) {
+  for (int s = 0; s < NP; ++s) {
     const float w = ls[s] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ls[s] - m_use);
     wsum += w;
     acc += ls[s] == -INFINITY ? f32x4{0.f, 0.f, 0.f, 0.f} : w * os[s];
@@ -173,12 +173,14 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
   const int app_blocks = (int)std::min<int64_t>((app_units + kMergeThreads - 1) / kMergeThreads, 2048);
   if (a.splits <= kFewParts) {
     const int blocks = (int)((rows * (a.D / 4) + kMergeThreads - 1) / kMergeThreads);
-    if (a.D == 128)
-      hipLaunchKernelGGL(attn_merge_rows_kernel<128>, dim3(blocks + app_blocks), dim3(kMergeThreads), 0, stream, a,
-                         blocks);
-    else
-      hipLaunchKernelGGL(attn_merge_rows_kernel<64>, dim3(blocks + app_blocks), dim3(kMergeThreads), 0, stream, a,
-                         blocks);
+    const dim3 grid(blocks + app_blocks), block(kMergeThreads);
+    if (a.splits <= 8) {
+      if (a.D == 128) hipLaunchKernelGGL((attn_merge_rows_kernel<128, 8>), grid, block, 0, stream, a, blocks);
+      else hipLaunchKernelGGL((attn_merge_rows_kernel<64, 8>), grid, block, 0, stream, a, blocks);
+    } else {
+      if (a.D == 128) hipLaunchKernelGGL((attn_merge_rows_kernel<128, 16>), grid, block, 0, stream, a, blocks);
+      else hipLaunchKernelGGL((attn_merge_rows_kernel<64, 16>), grid, block, 0, stream, a, blocks);
+    }
     return hipGetLastError();
   }
   // part groups: the parts rounded up to a power of two, at most what one row's

@@ -28,52 +28,58 @@ bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
 }
 
 struct Shape {
-  int C, S, R, Wv, ws, Hq, Hkv, D, splits, balanced, grid, bidir;
+  int C, S, R, Wv, ws, Hq, Hkv, D, splits, balanced, grid, bidir, pack;
   int64_t total_tiles;
   int64_t ws_bytes;
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
+// Row tiles of one head group: its C * pack packed rows ((token, query head)
+// pairs, token-major) in blocks of kBlockM.
+int64_t row_tiles(int C, int pack) { return (int64_t(C) * pack + vico::kBlockM - 1) / vico::kBlockM; }
+
 // Key tiles of row tile rt: up to its last row's last visible key (the
-// kernel's rule: the row's own position, or the chunk end when bidirectional).
-int64_t tiles_of(int rt, int C, int SW, int bidir) {
-  const int64_t last = bidir ? C : std::min<int64_t>(int64_t(rt + 1) * vico::kBlockM, C);
+// kernel's rule: the row's token position, or the chunk end when
+// bidirectional).  The last row of row tile rt is token ((rt+1)*kBlockM-1)/pack.
+int64_t tiles_of(int rt, int C, int SW, int bidir, int pack) {
+  const int64_t last =
+      bidir ? C : std::min<int64_t>((int64_t(rt + 1) * vico::kBlockM - 1) / pack + 1, C);
   return (SW + last + vico::kKeyTile - 1) / vico::kKeyTile;
 }
 
 // Splits of every row tile's key range: as many as keep the grid within one
 // round of resident work-groups (so that, e.g., 48 row tiles take 5 splits
-// and fill 240 of the 256 CUs), with at least 16 key tiles per split and at
-// most kAutoSplits.
-int plan_splits(int C, int S, int Wv, int Hq, int request) {
-  const int64_t n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
-  const int64_t wgs = int64_t(Hq) * n_rt;
+// and fill 240 of the 256 CUs), with at least kMinSplitTiles key tiles per
+// split and at most kAutoSplits.
+int plan_splits(int C, int S, int Wv, int Hq, int pack, int request) {
+  const int64_t wgs = int64_t(Hq / pack) * row_tiles(C, pack);
   const int64_t tiles = (int64_t(S) + Wv + C + vico::kKeyTile - 1) / vico::kKeyTile;
   const int64_t cap = tiles < vico::kMaxSplits ? tiles : vico::kMaxSplits;
   if (request > 0) return (int)(request < cap ? request : cap);
   int64_t ns = int64_t(vico::kNumCUs) * vico::kWgPerCU / wgs;
-  ns = std::min<int64_t>(std::min<int64_t>(ns, vico::kAutoSplits), std::min<int64_t>(cap, tiles / 16));
+  ns = std::min<int64_t>(std::min<int64_t>(ns, vico::kAutoSplits),
+                         std::min<int64_t>(cap, tiles / vico::kMinSplitTiles));
   return (int)std::max<int64_t>(ns, 1);
 }
 
 // Balanced plan: gridDim.x equal shares of the (row tile, key tile) pairs.
 // Returns the largest number of work-groups any row tile is spread over, or
 // 0 when the balanced schedule does not apply.
-int plan_balanced(int C, int SW, int Hq, int Hkv, int bidir, int64_t* total, int* grid) {
-  const int n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
-  const int g = Hq / Hkv;
+int plan_balanced(int C, int SW, int Hq, int Hkv, int bidir, int pack, int64_t* total, int* grid) {
+  const int n_rt = (int)row_tiles(C, pack);
+  const int gq = Hq / Hkv / pack;
   int64_t T = 0;
-  for (int rt = 0; rt < n_rt; ++rt) T += int64_t(Hq) * tiles_of(rt, C, SW, bidir);
+  for (int rt = 0; rt < n_rt; ++rt) T += int64_t(Hq / pack) * tiles_of(rt, C, SW, bidir, pack);
   const int64_t G = int64_t(vico::kNumCUs) * vico::kWgPerCU;
   if (T < 4 * G) return 0;
-  // walk the row tiles in kernel order: kv, row tile (longest first), query head
+  // walk the row tiles in kernel order: kv, row tile (longest first), head group
   int max_parts = 1;
   int64_t start = 0;
   for (int kv = 0; kv < Hkv; ++kv)
     for (int ri = 0; ri < n_rt; ++ri) {
-      const int64_t n = tiles_of(n_rt - 1 - ri, C, SW, bidir);
-      for (int qh = 0; qh < g; ++qh) {
+      const int64_t n = tiles_of(n_rt - 1 - ri, C, SW, bidir, pack);
+      for (int qh = 0; qh < gq; ++qh) {
         const int64_t w0 = ((start + 1) * G - 1) / T, w1 = ((start + n) * G - 1) / T;
         max_parts = (int)std::max<int64_t>(max_parts, w1 - w0 + 1);
         start += n;
@@ -105,26 +111,31 @@ int check_attn_shape(int32_t C, int32_t S, int32_t R, int64_t H, int64_t W, int3
   sh->ws = R > 0 ? (int)((H - wv) % R) : 0;
   sh->Hq = Hq; sh->Hkv = Hkv; sh->D = D;
   sh->bidir = bidir;
+  // Rows of a row tile: the tokens of one query head, or (token, query head)
+  // pairs of all query heads of a KV head when that takes fewer row tiles --
+  // a chunk of C tokens then leaves one part-filled row tile per KV head
+  // instead of one per query head.
+  sh->pack = row_tiles(C, Hq / Hkv) < int64_t(Hq / Hkv) * row_tiles(C, 1) ? Hq / Hkv : 1;
   sh->splits = 1;
   sh->balanced = 0;
   sh->total_tiles = 0;
   sh->grid = 0;
   if (C > 0) {
-    const int64_t n_rt = (C + vico::kBlockM - 1) / vico::kBlockM;
-    const int ns = splits == VICO_SPLIT_BALANCED ? 1 : plan_splits(C, S, (int)wv, Hq, splits);
+    const int64_t n_tiles_rows = int64_t(Hq / sh->pack) * row_tiles(C, sh->pack);   // row tiles, all heads
+    const int ns = splits == VICO_SPLIT_BALANCED ? 1 : plan_splits(C, S, (int)wv, Hq, sh->pack, splits);
     int parts = 0;
     // balanced when asked for, or when the split grid would leave at least half
     // the CUs idle (measured: with most CUs busy the merge costs what the
     // balance gains -- the chip runs power-limited and idle CUs raise the clock)
     if (splits == VICO_SPLIT_BALANCED ||
-        (splits == 0 && 2 * int64_t(Hq) * n_rt * ns <= int64_t(vico::kNumCUs) * vico::kWgPerCU))
-      parts = plan_balanced(C, S + (int)wv, Hq, Hkv, bidir, &sh->total_tiles, &sh->grid);
+        (splits == 0 && 2 * n_tiles_rows * ns <= int64_t(vico::kNumCUs) * vico::kWgPerCU))
+      parts = plan_balanced(C, S + (int)wv, Hq, Hkv, bidir, sh->pack, &sh->total_tiles, &sh->grid);
     if (parts > 0) {
       sh->balanced = 1;
       sh->splits = parts;
     } else {
       sh->splits = ns;
-      sh->grid = (int)(int64_t(Hq) * n_rt * ns);
+      sh->grid = (int)(n_tiles_rows * ns);
     }
   }
   sh->ws_bytes = sh->splits > 1
@@ -316,6 +327,7 @@ int vico_chunk_prefill_attn_ex(const void* q, const void* k_chunk, const void* v
   a.Hq = sh.Hq; a.Hkv = sh.Hkv; a.D = sh.D;
   a.splits = sh.splits;
   a.balanced = sh.balanced;
+  a.pack = sh.pack;
   a.total_tiles = sh.total_tiles;
   a.out_f32 = out_dtype == VICO_DTYPE_F32;
   a.bidir = sh.bidir;

@@ -7,8 +7,9 @@
 namespace vico {
 
 // Tile geometry of the attention kernel.  A work-group of 8 waves (two per
-// SIMD) owns kBlockM = 256 query rows of one query head; each wave owns
-// kRowBlocks = 1 block of 32 rows.  Keys are walked in tiles of kKeyTile,
+// SIMD) owns kBlockM = 256 query rows of one KV head: (token, query head)
+// pairs of its query heads, token-major; each wave owns kRowBlocks = 1 block
+// of 32 rows.  Keys are walked in tiles of kKeyTile,
 // double-buffered in LDS (32 KiB per 64 keys at head_dim 128); one
 // work-group per CU, so every K/V tile in LDS serves 256 rows.
 constexpr int kThreads = 512;
@@ -19,7 +20,8 @@ constexpr int kBuffers = 2;
 constexpr int kNumCUs = 256;        // MI355X: 8 XCDs x 32 CUs
 constexpr int kWgPerCU = 1;
 constexpr int kMaxSplits = 16;
-constexpr int kAutoSplits = 8;      // most key splits the planner picks by itself (the merge reads up to 8 parts at once)
+constexpr int kAutoSplits = 16;     // most key splits the planner picks by itself (the row merge reads up to 16 parts at once)
+constexpr int kMinSplitTiles = 8;   // fewest key tiles per split the planner picks by itself
 
 
 // Everything the attention kernels need, resolved on the host.
@@ -39,6 +41,8 @@ struct AttnArgs {
   int Hq, Hkv, D;
   int splits;          // partial results per row merged at the end (1: none)
   int balanced;        // 1: work-groups take equal shares of all key tiles
+  int pack;            // query heads packed into a row tile (divides Hq / Hkv): row r of a head
+                       // group is token r / pack of query head (group base) + r % pack
   int64_t total_tiles; // balanced mode: key tiles summed over all row tiles and heads
   int out_f32;
   int bidir;           // 1: every chunk row sees the whole chunk (no causal mask)
