@@ -125,10 +125,25 @@ def test_plan_for_the_workloads(cfg, splits):
                                           sh.num_q_heads, sh.num_kv_heads, sh.head_dim) == wb
 
 
+# 3B heads (16q/2kv) with a full 8192-token window, the 64-chunk stream's
+# shapes: a chunk length that is not a multiple of 256 is planned on packed
+# (token, head) row tiles, ceil(C * 8 / 256) per KV head, which leaves room for
+# more key splits in one round of 256 work-groups (at most 16, and at least 8
+# key tiles per split); whole 256-row tiles stay one query head per tile
+@pytest.mark.parametrize("C,splits", [(258, 14), (300, 12), (390, 9), (512, 8), (640, 6), (700, 5), (800, 5),
+                                      (1000, 4), (1024, 4)])
+def test_plan_for_ragged_stream_chunks(C, splits):
+    ns, wb = vico.vico_attn_plan(C, 64, 8192, 5 * 8192 + 777, 8192, 16, 2, 128)
+    assert ns == splits
+    assert wb == (4 * ns * 16 * C * 128 + 255) // 256 * 256 + 4 * ns * 16 * C
+
+
 def test_forced_splits_are_clamped_to_the_key_tiles():
     # 16 + 256 + 64 keys in tiles of 64 keys -> at most 6 splits
     assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=8)[0] == 6
     assert vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=2)[0] == 2
+    # and to 16 (the row merge loads up to 16 parts at once)
+    assert vico.vico_attn_plan(64, 16, 4096, 5000, 4096, 2, 1, 64, num_splits=40)[0] == 16
     with pytest.raises(vico.VicoError):
         vico.vico_attn_plan(64, 16, 256, 456, 256, 2, 1, 64, num_splits=-3)
 
