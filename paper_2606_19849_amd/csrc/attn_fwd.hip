@@ -10,12 +10,13 @@
 //   * Work-group = 8 waves (two per SIMD, one work-group per CU) = 256 query
 //     rows (one key range when split).  Each wave owns 32 rows for the whole
 //     key loop; every K/V tile brought into LDS serves all 256 rows.  The
-//     rows are 256 tokens of one query head, or -- when the chunk length is
-//     not a multiple of 256, so that the last row tile of every query head
-//     would be part-empty -- packed (token, head) pairs of all query heads of
-//     one KV head, token-major (row r: token r / g, head kv*g + r % g), which
-//     leaves one part-filled row tile per KV head instead.  Both forms read
-//     the same K/V; the packed one is its own kernel, attn_fwd_packed_kernel.
+//     rows are 256 tokens of one query head, or packed (token, head) pairs
+//     of all query heads of one KV head, token-major (row r: token r / g,
+//     head kv*g + r % g) when that takes fewer row tiles: a chunk length
+//     that is not a multiple of 256 leaves every query head's last row tile
+//     part-empty, and packing leaves one part-filled row tile per KV head
+//     instead.  Both forms read the same K/V; the packed one is its own
+//     kernel, attn_fwd_packed_kernel.
 //   * The tile body (S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_32x32x16_bf16,
 //     the exponentiate-first online softmax, two 32-key halves) is WaveTile
 //     of attn_common.h, shared with the gathered-query kernel.

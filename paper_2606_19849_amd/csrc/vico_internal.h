@@ -7,9 +7,9 @@
 namespace vico {
 
 // Tile geometry of the attention kernel.  A work-group of 8 waves (two per
-// SIMD) owns kBlockM = 256 query rows of one KV head: (token, query head)
-// pairs of its query heads, token-major; each wave owns kRowBlocks = 1 block
-// of 32 rows.  Keys are walked in tiles of kKeyTile,
+// SIMD) owns kBlockM = 256 query rows -- tokens of one query head, or packed
+// (token, query head) pairs of the query heads of one KV head, token-major;
+// each wave owns kRowBlocks = 1 block of 32 rows.  Keys are walked in tiles of kKeyTile,
 // double-buffered in LDS (32 KiB per 64 keys at head_dim 128); one
 // work-group per CU, so every K/V tile in LDS serves 256 rows.
 constexpr int kThreads = 512;
