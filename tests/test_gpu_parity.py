@@ -62,6 +62,46 @@ def test_small_f2_fp32(name, splits):
     check_f32(o, ref, b, lse, ref_lse)
 
 
+def _ragged_gqa_shapes(n=12, seed=2024):
+    """Seeded shapes with more than one query head per KV head and chunk
+    lengths that are not a multiple of 256, so most are planned on packed
+    (token, head) row tiles: GQA ratios 2-8, head_dim 64 and 128, windows that
+    wrap the ring, and the split modes auto, none, 5, 16 and balanced."""
+    rng = np.random.default_rng(seed)
+    shapes = []
+    for _ in range(n):
+        hkv = int(rng.choice([1, 2]))
+        g = int(rng.integers(2, 9))
+        d = int(rng.choice([64, 128]))
+        c = int(rng.integers(1, 400))
+        r = int(rng.integers(64, 1000))
+        w = int(rng.integers(0, r + 1))
+        shapes.append((ChunkShape(hkv * g, hkv, d, int(rng.integers(0, 80)), r, int(rng.integers(w, 4 * r)), w, c),
+                       int(rng.choice([0, 1, 5, 16, -1]))))
+    return shapes
+
+
+RAGGED_GQA = _ragged_gqa_shapes()
+
+
+def test_ragged_gqa_shapes_are_mostly_packed():
+    """(host check of the case list) packing takes fewer row tiles than one
+    query head per row tile for most of the cases below"""
+    packed = [-(-sh.chunk_len * (sh.num_q_heads // sh.num_kv_heads) // 256) <
+              (sh.num_q_heads // sh.num_kv_heads) * -(-sh.chunk_len // 256) for sh, _ in RAGGED_GQA]
+    assert sum(packed) >= len(packed) // 2
+
+
+@pytest.mark.parametrize("case", range(len(RAGGED_GQA)))
+def test_ragged_gqa_f2_fp32(case):
+    sh, splits = RAGGED_GQA[case]
+    inp = make_chunk_inputs(sh, seed=300 + case, family="F2")
+    dc = DeviceChunk(inp)
+    o, lse = dc.attention(torch.float32, num_splits=splits)
+    ref, ref_lse, b = oracle_and_bound(inp, parts=dc.parts)
+    check_f32(o, ref, b, lse, ref_lse)
+
+
 @pytest.mark.parametrize("name", sorted(SMALL))
 def test_small_f2_bf16(name):
     inp = make_chunk_inputs(SMALL[name], seed=102, family="F2")
