@@ -37,7 +37,8 @@ PEAK_HBM_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 CSRC = "paper_2606_19849_amd/csrc/"
 # sources whose kernels a traffic figure covers (it goes stale when any changes)
-KERNEL_SRC = {"attn_fwd_kernel<128>": [CSRC + "attn_fwd.hip", CSRC + "attn_common.h", CSRC + "vico_internal.h"],
+KERNEL_SRC = {"attn_fwd_kernel<128>": [CSRC + "attn_fwd.hip", CSRC + "attn_merge.hip", CSRC + "attn_common.h",
+                                       CSRC + "vico_internal.h"],
               "attn_gather_kernel<128>": [CSRC + "attn_gather.hip", CSRC + "attn_merge.hip", CSRC + "attn_common.h",
                                           CSRC + "vico_internal.h"],
               "kv_append_kernel": [CSRC + "kv_append.hip"],

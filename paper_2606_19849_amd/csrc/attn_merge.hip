@@ -49,7 +49,8 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_rows_kernel(AttnArgs
   const int dq = (int)(idx % NQ);
   const int64_t hr = idx / NQ;
   // every part's lse and O of this thread are loaded together (NP >= the
-  // parts, unrolled), so one memory latency covers the whole row.  The O
+  // parts, unrolled; the launch takes the smallest of 2, 4, 8, 16 that
+  // covers them), so one memory latency covers the whole row.  The O
   // loads do not wait for the lse values: a part past the last reads the last
   // part's slot, and an empty part (lse = -inf, its O slot possibly never
   // written) is dropped by the select in the sum, whatever its slot holds.
@@ -174,7 +175,13 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t stream) {
   if (a.splits <= kFewParts) {
     const int blocks = (int)((rows * (a.D / 4) + kMergeThreads - 1) / kMergeThreads);
     const dim3 grid(blocks + app_blocks), block(kMergeThreads);
-    if (a.splits <= 8) {
+    if (a.splits <= 2) {
+      if (a.D == 128) hipLaunchKernelGGL((attn_merge_rows_kernel<128, 2>), grid, block, 0, stream, a, blocks);
+      else hipLaunchKernelGGL((attn_merge_rows_kernel<64, 2>), grid, block, 0, stream, a, blocks);
+    } else if (a.splits <= 4) {
+      if (a.D == 128) hipLaunchKernelGGL((attn_merge_rows_kernel<128, 4>), grid, block, 0, stream, a, blocks);
+      else hipLaunchKernelGGL((attn_merge_rows_kernel<64, 4>), grid, block, 0, stream, a, blocks);
+    } else if (a.splits <= 8) {
       if (a.D == 128) hipLaunchKernelGGL((attn_merge_rows_kernel<128, 8>), grid, block, 0, stream, a, blocks);
       else hipLaunchKernelGGL((attn_merge_rows_kernel<64, 8>), grid, block, 0, stream, a, blocks);
     } else {
