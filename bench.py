@@ -452,17 +452,22 @@ def run_stream_workload(args, torch, vico):
             vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, int(starts[t]), window, outs[t],
                                          workspace=ws, stream=stream, flags=vico.VICO_ATTN_APPEND)
 
+        hold_ms = 6.0
         while n_warm is None or rep < n_warm + args.steps:
             if n_warm is None and rep >= args.warmup and time.perf_counter() - t_warm >= args.warmup_seconds:
                 n_warm = rep
             ends = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            busy.hold(stream, ms=6.0)
+            busy.hold(stream, ms=hold_ms)
             ends[0].record(stream)
+            t_host = time.perf_counter()
             for t in range(len(counts)):
                 chunk(t)
+            # the hold must outlast the host's enqueueing of the 64 calls, or
+            # the GPU would wait for the host inside the timed span
+            hold_ms = max(hold_ms, 1.5e3 * (time.perf_counter() - t_host))
             ends[1].record(stream)
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(counts) + 1)]
-            busy.hold(stream, ms=6.0)
+            busy.hold(stream, ms=hold_ms)
             ev[0].record(stream)
             for t in range(len(counts)):
                 chunk(t)
