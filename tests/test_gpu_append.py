@@ -107,3 +107,62 @@ def test_attention_with_append_equals_attention_then_append(splits, flags):
         mv.append(vb, H)
         assert np.array_equal(bits_of(rk_b), mk.buf) and np.array_equal(bits_of(rv_b), mv.buf)
         H += c
+
+
+@pytest.mark.parametrize("C,splits", [(300, 0), (513, 3), (1024, 0)])
+def test_chunk_call_with_append_replays_as_a_graph(C, splits):
+    """A chunk call with VICO_ATTN_APPEND (attention, the split merge and the
+    ring copy riding on it; a 300-token chunk runs the packed row tiles)
+    captured into a HIP graph replays the eager result bit for bit, replay
+    after replay, with an eager call of another window on the same buffers in
+    between.  The window and the appended slots do not overlap (W + C <= R),
+    so every replay sees the same window and writes the same slots."""
+    Hq, Hkv, D, S, R, W, W2 = 8, 2, 128, 16, 2048, 900, 300
+    assert W + C <= R
+    rng = np.random.default_rng(C + splits)
+    sk, sv = dev(_rand_bits(rng, (S, Hkv, D))), dev(_rand_bits(rng, (S, Hkv, D)))
+    ring0 = _rand_bits(rng, (R, Hkv, D))
+    rk, rv = dev(ring0), dev(ring0.copy())
+    q, k, v = (dev(_rand_bits(rng, (C, Hq, D))), dev(_rand_bits(rng, (C, Hkv, D))),
+               dev(_rand_bits(rng, (C, Hkv, D))))
+    H = 3 * R + 555
+    parts, wb = vico.vico_attn_plan(C, S, R, H, W, Hq, Hkv, D, splits, vico.VICO_ATTN_APPEND)
+    assert parts > 1                  # the merge (and the append on it) is part of the graph
+    ws = torch.empty(max(wb, vico.vico_attn_plan(C, S, R, H, W2, Hq, Hkv, D)[1]), dtype=torch.uint8, device="cuda")
+    out = torch.empty((C, Hq, D), dtype=torch.float32, device="cuda")
+    lse = torch.empty((Hq, C), dtype=torch.float32, device="cuda")
+
+    def call(window, flags):
+        vico.vico_chunk_prefill_attn(q, k, v, sk, sv, rk, rv, H, window, out, lse=lse, workspace=ws,
+                                     num_splits=splits if window == W else 0, flags=flags)
+
+    call(W, vico.VICO_ATTN_APPEND)
+    torch.cuda.synchronize()
+    eager = (out.clone(), lse.clone(), rk.clone(), rv.clone())
+    mk = oracle.RingModel(R, (Hkv, D))
+    mk.buf[:] = ring0
+    mk.append(bits_of(k), H)
+    assert np.array_equal(bits_of(rk), mk.buf)
+    call(W2, 0)
+    torch.cuda.synchronize()
+    other = (out.clone(), lse.clone())
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        call(W, vico.VICO_ATTN_APPEND)        # warm-up on the capture stream
+        torch.cuda.current_stream().synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            call(W, vico.VICO_ATTN_APPEND)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        call(W2, 0)                           # eager call of another window, same buffers
+        torch.cuda.synchronize()
+        assert torch.equal(out, other[0]) and torch.equal(lse, other[1])
+        out.zero_()
+        lse.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager[0]) and torch.equal(lse, eager[1])
+        assert torch.equal(rk, eager[2]) and torch.equal(rv, eager[3])
