@@ -18,7 +18,10 @@ decode step over them; drop = temporal token dropping of a batch of chunks).
 Prints one JSON line.  `value` is algorithmic TFLOP/s over whole steps
 (attention + append); `roofline` prices the attention kernel alone from
 HIP events on its stream; `cpu_baseline` times the fp64 oracle on a bounded
-sample of rows of the same chunk on the host cores.
+sample of rows of the same chunk on the host cores.  The short-call
+workloads (query, decode, drop, append) and the stream's aggregate rate are
+timed over K calls launched back to back, with events only at the two ends;
+their per-call event figures are printed beside them.
 """
 from __future__ import annotations
 
