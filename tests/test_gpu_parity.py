@@ -23,6 +23,7 @@ import numpy as np
 import pytest
 import torch
 
+import paper_2606_19849_amd as vico
 from oracle import bf16_bits_to_f64
 from synth import CONFIGS, ChunkShape, f32_to_bf16_bits, make_chunk_inputs
 from tests._gpu import (DeviceChunk, check_bf16, check_f1, check_f32, check_literal, check_relative,
@@ -93,12 +94,16 @@ def test_ragged_gqa_shapes_are_mostly_packed():
 
 
 @pytest.mark.parametrize("case", range(len(RAGGED_GQA)))
-def test_ragged_gqa_f2_fp32(case):
+@pytest.mark.parametrize("bidir", [False, True])
+def test_ragged_gqa_f2_fp32(case, bidir):
+    """The seeded ragged GQA shapes, causal and with the bidirectional
+    in-chunk option (every row sees the whole chunk)."""
     sh, splits = RAGGED_GQA[case]
     inp = make_chunk_inputs(sh, seed=300 + case, family="F2")
     dc = DeviceChunk(inp)
-    o, lse = dc.attention(torch.float32, num_splits=splits)
-    ref, ref_lse, b = oracle_and_bound(inp, parts=dc.parts)
+    flags = vico.VICO_ATTN_BIDIRECTIONAL if bidir else 0
+    o, lse = dc.attention(torch.float32, num_splits=splits, flags=flags)
+    ref, ref_lse, b = oracle_and_bound(inp, parts=dc.parts, bidirectional=bidir)
     check_f32(o, ref, b, lse, ref_lse)
 
 
@@ -220,7 +225,6 @@ def test_no_lse_and_side_stream_give_the_same_output(splits):
     """The LSE output is optional: without it the output is bit-identical
     (also through the split merge).  The library runs on the caller's stream:
     attention and append issued on a side stream give bit-identical results."""
-    import paper_2606_19849_amd as vico
     inp = make_chunk_inputs(SMALL["gqa7_ragged"], seed=110, family="F2")
     dc = DeviceChunk(inp)
     o_lse, _ = dc.attention(torch.float32, num_splits=splits)
@@ -274,7 +278,6 @@ def test_balanced_schedule_agrees_on_every_row(cfg):
     log-sum-exp) against the default one, on every row and head, within the
     sum of the two results' derived bounds (sum p|v|/l from the oracle over
     |V| for all rows)."""
-    import paper_2606_19849_amd as vico
     from tests._bounds import chunk_bound
     from tests._util import to_f64
     sh = CONFIGS[cfg]
@@ -359,7 +362,6 @@ def test_ring_at_the_32bit_offset_limit():
     read changes the mean.  The window leaves 100000 slots out and wraps at the
     ring end; the slots nearest 2^31 bytes are read.  An append across the
     ring end then lands bit-exact."""
-    import paper_2606_19849_amd as vico
     Hq, Hkv, D, S, C = 2, 1, 128, 16, 64
     R = (1 << 31) // (Hkv * D * 2) - 1
     H = R + 777
